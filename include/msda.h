@@ -1,0 +1,118 @@
+/*
+ * libmsda: multi-scale deformable attention (MSDA), forward and backward, for AMD MI355X (gfx950).
+ *
+ * The operation (paper: "Towards Efficient Multi-Scale Deformable Attention on NPU", Sec. 3 and
+ * Sec. 4). Every query q of batch n and head m samples each of L feature levels at P learned
+ * locations. Each sample is a bilinear interpolation over the 2x2 pixel neighbourhood of the
+ * location (Sec. 3); the samples are multiplied by their attention weights and summed over levels
+ * and points (Sec. 4, first paragraph). The backward pass returns the gradients w.r.t. the
+ * sampling locations and the attention weights, and w.r.t. the value tensor by scatter-add
+ * (Sec. 4.2). Sampling follows the grid-sample convention the paper takes its reference
+ * implementation from (Sec. 3, Fig. 3): locations are normalized to [0,1] per level,
+ * align_corners=False, and reads off the map are zero.
+ *
+ *   w_im = fmaf(x, W_l, -0.5f), h_im = fmaf(y, H_l, -0.5f)   (fp32, one rounding)
+ *   a sample is used only if -1 < h_im < H_l and -1 < w_im < W_l; corners off the map read 0
+ *   out[n,q,m*D+d] = sum_{l,p} attn[n,q,m,l,p] * bilinear(value[n, level l, m, d], h_im, w_im)
+ *
+ * Tensor layouts (row-major, C order):
+ *   value        [N, S, M, D]        dtype (fp32 or fp16); S = sum_l H_l*W_l; pixel (h,w) of level l
+ *                                    is row level_start_index[l] + h*W_l + w
+ *   spatial_shapes    [L, 2] int64 (H_l, W_l)       HOST memory
+ *   level_start_index [L]    int64                  HOST memory; must equal the prefix sums of H*W
+ *   sampling_loc [N, Lq, M, L, P, 2] fp32, (x, y) normalized: x scales with W_l, y with H_l
+ *   attn_weight  [N, Lq, M, L, P]    fp32 (used as given; no normalization is assumed)
+ *   out          [N, Lq, M*D]        dtype
+ *   grad_out     [N, Lq, M*D]        dtype
+ *   grad_value   [N, S, M, D]        fp32 (also for fp16 value)
+ *   grad_loc     [N, Lq, M, L, P, 2] fp32
+ *   grad_attn    [N, Lq, M, L, P]    fp32
+ *
+ * Ownership and execution. All tensor pointers are DEVICE pointers owned by the caller, except the
+ * two level tables, which are HOST pointers read during the call. The library allocates no memory,
+ * keeps no state between calls, never synchronizes and never prints. Work is enqueued on `stream`
+ * (a hipStream_t; NULL means the default stream) and the call returns before it completes.
+ * Outputs are overwritten entirely and must not alias inputs. Inputs are not modified.
+ * Arithmetic is fp32 (fp16 inputs are converted exactly; fp16 out is rounded to nearest-even
+ * once). grad_value is accumulated with fp32 atomics, so its low bits depend on the order in
+ * which additions land.
+ *
+ * Errors are returned, never raised: nothing is launched when a check fails, and
+ * msda_last_error() then describes the failed check (thread-local, valid until the next call on
+ * the same thread).
+ */
+#ifndef MSDA_H_
+#define MSDA_H_
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Largest number of feature levels L accepted. */
+#define MSDA_MAX_LEVELS 16
+
+typedef enum {
+    MSDA_SUCCESS = 0,
+    MSDA_ERROR_INVALID_VALUE = 1, /* null pointer with nonzero extent, bad size, inconsistent level table,
+                                     misaligned pointer, unknown dtype                                   */
+    MSDA_ERROR_NOT_SUPPORTED = 2, /* valid request beyond this build's limits (L > MSDA_MAX_LEVELS, a
+                                     tensor of 2^29 elements or more per batch item, D > 4096)          */
+    MSDA_ERROR_LAUNCH_FAILED = 3  /* the HIP runtime reported an error when the kernels were enqueued */
+} msda_status_t;
+
+/* Element type of value, out and grad_out. */
+typedef enum { MSDA_F32 = 0, MSDA_F16 = 1 } msda_dtype_t;
+
+/*
+ * Validate a problem description without touching any device: sizes, dtype and the level table.
+ * Checks: N, Lq >= 0; M, D, L, P >= 1; L <= MSDA_MAX_LEVELS; H_l, W_l >= 1;
+ * level_start_index[l] == sum_{l' < l} H_l' * W_l'; S == sum_l H_l * W_l; size limits.
+ * spatial_shapes and level_start_index are host pointers and must be non-null.
+ */
+msda_status_t msda_check_args(const int64_t* spatial_shapes, const int64_t* level_start_index,
+                              int64_t N, int64_t S, int64_t M, int64_t D, int64_t Lq, int64_t L,
+                              int64_t P, int dtype);
+
+/*
+ * Forward pass (Sec. 4.1): out = MSDA(value, sampling_loc, attn_weight).
+ * value and out must be 16-byte aligned; sampling_loc 8-byte; attn_weight 4-byte.
+ * N*Lq == 0 is a successful no-op.
+ */
+msda_status_t msda_forward(const void* value, const int64_t* spatial_shapes,
+                           const int64_t* level_start_index, const float* sampling_loc,
+                           const float* attn_weight, void* out,
+                           int64_t N, int64_t S, int64_t M, int64_t D, int64_t Lq, int64_t L,
+                           int64_t P, int dtype, void* stream);
+
+/*
+ * Backward pass (Sec. 4.2): given grad_out = dLoss/dout, write
+ *   grad_value = dLoss/dvalue (zeroed, then accumulated by scatter-add),
+ *   grad_loc   = dLoss/dsampling_loc, grad_attn = dLoss/dattn_weight.
+ * At an integer h_im (or w_im) the location gradient is the one of the cell [floor, floor+1];
+ * samples outside the open range above get zero location and weight gradients.
+ * value and grad_out 16-byte aligned; grad_value 16-byte; grad_loc 8-byte; grad_attn 4-byte.
+ * N*Lq == 0 still zeroes grad_value.
+ */
+msda_status_t msda_backward(const void* value, const int64_t* spatial_shapes,
+                            const int64_t* level_start_index, const float* sampling_loc,
+                            const float* attn_weight, const void* grad_out, float* grad_value,
+                            float* grad_loc, float* grad_attn,
+                            int64_t N, int64_t S, int64_t M, int64_t D, int64_t Lq, int64_t L,
+                            int64_t P, int dtype, void* stream);
+
+/* Static name of a status code ("MSDA_SUCCESS", ...). */
+const char* msda_status_string(msda_status_t status);
+
+/* Description of the last failed check or launch on the calling thread ("" if none). */
+const char* msda_last_error(void);
+
+/* Library version as major*10000 + minor*100 + patch. */
+int msda_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MSDA_H_ */

@@ -1,0 +1,500 @@
+// MSDA forward and backward kernels for gfx950 (CDNA4, wave64).
+//
+// The operation is the one of the paper's Sec. 3-4: per (query, head) pair, L*P bilinear samples
+// of the value tensor, weighted by attention weights and summed (forward); the gradients w.r.t.
+// locations, weights (reductions over channels) and value (scatter-add) (backward, Sec. 4.2).
+//
+// Mapping (shared by both passes):
+//   * A workgroup of 256 lanes owns one (batch n, head m) pair and a run of consecutive queries,
+//     so every value / grad_value row it touches lies in that head's slab. Workgroups are
+//     renumbered so that all the work of one (n, m) slab lands on one XCD (consecutive workgroup
+//     ids are dealt round-robin to the 8 XCDs): the slab's value lines stay in one XCD's L2 and
+//     grad_value atomics on a line come from one L2.
+//   * Within a wave, LPP lanes serve one query; each lane owns VEC contiguous channels, so one
+//     corner of one sample is a single coalesced row read (D=32 fp32: 8 lanes x 16 B = 128 B).
+//     A wave serves 64/LPP queries at once.
+//   * Phase 1: the wave computes the per-sample work (coordinates, range test, floor, the four
+//     corner rows and bilinear weights) once per sample, one sample per lane, and parks it in
+//     LDS. Phase 2: every lane of a query walks that query's samples, reading the parked
+//     description with a broadcast LDS read and gathering the four corner rows.
+//   * Off-map corners carry an out-of-range buffer offset: the buffer load returns zero and the
+//     buffer atomic is dropped by the hardware, with no branch.
+#include <hip/hip_runtime.h>
+
+#include "msda_internal.h"
+
+namespace msda {
+namespace {
+
+constexpr int kBlock = 256;
+constexpr int kWaves = kBlock / 64;
+constexpr int kMaxItems = 128;  // (query, sample) items parked in LDS per wave per phase
+constexpr uint32_t kOOBElem = uint32_t(kMaxLaunchElems);
+constexpr int kBufFlags = 0x00020000;  // buffer resource word 3 for gfx9: 32-bit data format
+
+using rsrc_t = __amdgpu_buffer_rsrc_t;
+
+__device__ __forceinline__ rsrc_t make_rsrc(const void* p, uint32_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, (int)bytes, kBufFlags);
+}
+
+// Orders a wave's LDS writes before other lanes of the same wave read them (and the reverse).
+__device__ __forceinline__ void wave_lds_sync() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0)
+    __builtin_amdgcn_wave_barrier();
+}
+
+// ---------------------------------------------------------------- row loads / stores
+
+// Reinterpret one 32-bit word as fp32. Elements of a loaded vector are copied into a scalar
+// first: clang lowers __builtin_bit_cast applied directly to a vector-element expression as a
+// read of element 0.
+__device__ __forceinline__ float as_float(uint32_t u) { return __builtin_bit_cast(float, u); }
+
+template <typename T, int VEC>
+struct Row;
+
+template <int VEC>
+struct Row<float, VEC> {
+    static constexpr int kShift = 2;
+    static __device__ __forceinline__ void load(float (&v)[VEC], rsrc_t r, uint32_t off) {
+        if constexpr (VEC == 4) {
+            auto x = __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const uint32_t u = x[i];
+                v[i] = as_float(u);
+            }
+        } else if constexpr (VEC == 2) {
+            auto x = __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, 0);
+            const uint32_t u0 = x[0], u1 = x[1];
+            v[0] = as_float(u0);
+            v[1] = as_float(u1);
+        } else {
+            static_assert(VEC == 1, "fp32 rows are read 1, 2 or 4 channels per lane");
+            v[0] = as_float(__builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 0));
+        }
+    }
+    static __device__ __forceinline__ void load_ptr(float (&v)[VEC], const float* p) {
+#pragma unroll
+        for (int i = 0; i < VEC; ++i) v[i] = p[i];
+    }
+    static __device__ __forceinline__ void store(float* p, const float (&v)[VEC]) {
+        if constexpr (VEC == 4) {
+            *reinterpret_cast<float4*>(p) = make_float4(v[0], v[1], v[2], v[3]);
+        } else if constexpr (VEC == 2) {
+            *reinterpret_cast<float2*>(p) = make_float2(v[0], v[1]);
+        } else {
+            p[0] = v[0];
+        }
+    }
+};
+
+typedef _Float16 half2_t __attribute__((ext_vector_type(2)));
+
+__device__ __forceinline__ void unpack_h2(uint32_t u, float& a, float& b) {
+    half2_t h = __builtin_bit_cast(half2_t, u);
+    a = (float)h[0];
+    b = (float)h[1];
+}
+
+__device__ __forceinline__ uint32_t pack_h2(float a, float b) {
+    half2_t h;
+    h[0] = (_Float16)a;  // round to nearest even
+    h[1] = (_Float16)b;
+    return __builtin_bit_cast(uint32_t, h);
+}
+
+template <int VEC>
+struct Row<_Float16, VEC> {
+    static constexpr int kShift = 1;
+    static __device__ __forceinline__ void load(float (&v)[VEC], rsrc_t r, uint32_t off) {
+        if constexpr (VEC == 8) {
+            auto x = __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const uint32_t u = x[i];
+                unpack_h2(u, v[2 * i], v[2 * i + 1]);
+            }
+        } else if constexpr (VEC == 4) {
+            auto x = __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, 0);
+            const uint32_t u0 = x[0], u1 = x[1];
+            unpack_h2(u0, v[0], v[1]);
+            unpack_h2(u1, v[2], v[3]);
+        } else if constexpr (VEC == 2) {
+            unpack_h2(__builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 0), v[0], v[1]);
+        } else {
+            static_assert(VEC == 1, "fp16 rows are read 1, 2, 4 or 8 channels per lane");
+            const uint16_t u = __builtin_amdgcn_raw_buffer_load_b16(r, off, 0, 0);
+            v[0] = (float)__builtin_bit_cast(_Float16, u);
+        }
+    }
+    static __device__ __forceinline__ void load_ptr(float (&v)[VEC], const _Float16* p) {
+#pragma unroll
+        for (int i = 0; i < VEC; ++i) v[i] = (float)p[i];
+    }
+    static __device__ __forceinline__ void store(_Float16* p, const float (&v)[VEC]) {
+        if constexpr (VEC == 8) {
+            uint4 u = make_uint4(pack_h2(v[0], v[1]), pack_h2(v[2], v[3]), pack_h2(v[4], v[5]),
+                                 pack_h2(v[6], v[7]));
+            *reinterpret_cast<uint4*>(p) = u;
+        } else if constexpr (VEC == 4) {
+            *reinterpret_cast<uint2*>(p) = make_uint2(pack_h2(v[0], v[1]), pack_h2(v[2], v[3]));
+        } else if constexpr (VEC == 2) {
+            *reinterpret_cast<uint32_t*>(p) = pack_h2(v[0], v[1]);
+        } else {
+            p[0] = (_Float16)v[0];
+        }
+    }
+};
+
+// ---------------------------------------------------------------- reductions over a lane group
+
+template <int CTRL>
+__device__ __forceinline__ float dpp(float v) {
+    return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), CTRL,
+                                                                 0xf, 0xf, false));
+}
+
+// Sum over the LPP consecutive lanes of a group; every lane of the group gets the total.
+// Steps 1-2 swap within quads (quad_perm), step 3 mirrors within 8 lanes (each lane meets the
+// other quad), step 4 mirrors within 16 lanes (each lane meets the other 8), then bpermute.
+template <int LPP>
+__device__ __forceinline__ float group_sum(float v) {
+    if constexpr (LPP >= 2) v += dpp<0xB1>(v);   // quad_perm [1,0,3,2]
+    if constexpr (LPP >= 4) v += dpp<0x4E>(v);   // quad_perm [2,3,0,1]
+    if constexpr (LPP >= 8) v += dpp<0x141>(v);  // row_half_mirror
+    if constexpr (LPP >= 16) v += dpp<0x140>(v); // row_mirror
+    if constexpr (LPP >= 32) v += __shfl_xor(v, 16, 64);
+    if constexpr (LPP >= 64) v += __shfl_xor(v, 32, 64);
+    return v;
+}
+
+// ---------------------------------------------------------------- work decomposition
+
+struct Tile {
+    int n, m, q0;  // slab (n, m) and the first query of this wave
+};
+
+// Workgroup -> (slab, query chunk). The grid is a multiple of 8; workgroup b runs on XCD b % 8,
+// and XCD x receives the contiguous range of work items [x*G/8, (x+1)*G/8) in slab-major order.
+__device__ __forceinline__ bool tile_of(const Params& p, int PPW, Tile& t) {
+    const uint32_t G = gridDim.x;
+    const uint32_t b = blockIdx.x;
+    const uint32_t w = (b & 7u) * (G >> 3) + (b >> 3);
+    if (w >= (uint32_t)p.num_blocks) return false;
+    const int slab = (int)(w / (uint32_t)p.chunks);
+    const int chunk = (int)(w - (uint32_t)slab * (uint32_t)p.chunks);
+    t.n = slab / p.M;
+    t.m = slab - t.n * p.M;
+    t.q0 = chunk * p.q_per_block + (int)(threadIdx.x >> 6) * PPW;
+    return true;
+}
+
+// Per-sample description computed in phase 1.
+struct SampleDesc {
+    int4 off;    // element offsets of the four corner rows (channel 0), or kOOBElem
+    float4 w;    // bilinear weights of the corners (00, 01, 10, 11), times `scale`
+    float a, lh, lw;
+};
+
+// Coordinates, range test, floor and corner rows of one sample (Sec. 3: the 2x2 neighbourhood).
+// h_im / w_im are formed with one fp32 rounding, so floor() decisions are reproducible.
+__device__ __forceinline__ void describe(const Params& p, const int* s_lvl, int n, int m, int q, int k,
+                                         bool fold_attn, SampleDesc& sd) {
+    sd.off = make_int4(kOOBElem, kOOBElem, kOOBElem, kOOBElem);
+    sd.w = make_float4(0.f, 0.f, 0.f, 0.f);
+    sd.a = 0.f;
+    sd.lh = 0.f;
+    sd.lw = 0.f;
+    if (q >= p.Lq) return;
+    const int l = k / p.P;
+    const int H = s_lvl[l], W = s_lvl[kMaxLevels + l], st = s_lvl[2 * kMaxLevels + l];
+    const int smp = ((n * p.Lq + q) * p.M + m) * p.K + k;
+    const float2 xy = reinterpret_cast<const float2*>(p.loc)[smp];
+    const float a = p.attn[smp];
+    const float Hf = (float)H, Wf = (float)W;
+    const float w_im = __builtin_fmaf(xy.x, Wf, -0.5f);
+    const float h_im = __builtin_fmaf(xy.y, Hf, -0.5f);
+    if (!(h_im > -1.f && w_im > -1.f && h_im < Hf && w_im < Wf)) return;
+    const float h0f = floorf(h_im), w0f = floorf(w_im);
+    const int h0 = (int)h0f, w0 = (int)w0f;
+    const float lh = h_im - h0f, lw = w_im - w0f;
+    const float hh = 1.f - lh, hw = 1.f - lw;
+    const float s = fold_attn ? a : 1.f;
+    sd.w = make_float4(s * (hh * hw), s * (hh * lw), s * (lh * hw), s * (lh * lw));
+    sd.a = a;
+    sd.lh = lh;
+    sd.lw = lw;
+    const bool top = h0 >= 0, bot = h0 + 1 < H, lef = w0 >= 0, rig = w0 + 1 < W;
+    // element offset of pixel (h0, w0) of this slab; corners add 0, 1, W, W+1 pixels
+    const int base = ((n * p.S + st + h0 * W + w0) * p.M + m) * p.D;
+    const int step_w = p.M * p.D, step_h = W * p.M * p.D;
+    sd.off.x = (top && lef) ? base : (int)kOOBElem;
+    sd.off.y = (top && rig) ? base + step_w : (int)kOOBElem;
+    sd.off.z = (bot && lef) ? base + step_h : (int)kOOBElem;
+    sd.off.w = (bot && rig) ? base + step_h + step_w : (int)kOOBElem;
+}
+
+__device__ __forceinline__ void load_levels(const Params& p, int* s_lvl) {
+    if (threadIdx.x < kMaxLevels) {
+        const int l = threadIdx.x;
+        s_lvl[l] = l < p.L ? p.H[l] : 1;
+        s_lvl[kMaxLevels + l] = l < p.L ? p.W[l] : 1;
+        s_lvl[2 * kMaxLevels + l] = l < p.L ? p.start[l] : 0;
+    }
+    __syncthreads();
+}
+
+// ---------------------------------------------------------------- forward
+
+template <typename T, int VEC, int LPP>
+__global__ __launch_bounds__(kBlock) void fwd_kernel(Params p) {
+    constexpr int PPW = 64 / LPP;
+    __shared__ int s_lvl[3 * kMaxLevels];
+    __shared__ int4 s_off[kWaves][kMaxItems];
+    __shared__ float4 s_w[kWaves][kMaxItems];
+    load_levels(p, s_lvl);
+
+    Tile t;
+    if (!tile_of(p, PPW, t)) return;
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    const int ps = lane / LPP, sub = lane % LPP;
+    const int q_mine = t.q0 + ps;
+    const int K = p.K;
+    const int KC = K < kMaxItems / PPW ? K : kMaxItems / PPW;
+    const rsrc_t vr = make_rsrc(p.value, p.value_bytes);
+    T* out = static_cast<T*>(p.out);
+
+    for (int c0 = 0; c0 < p.D; c0 += LPP * VEC) {
+        const int chan = c0 + sub * VEC;
+        const bool active = chan < p.D;
+        const uint32_t chan_bytes = (uint32_t)chan << Row<T, VEC>::kShift;
+        float acc[VEC];
+#pragma unroll
+        for (int i = 0; i < VEC; ++i) acc[i] = 0.f;
+
+        for (int k0 = 0; k0 < K; k0 += KC) {
+            const int kn = K - k0 < KC ? K - k0 : KC;
+            wave_lds_sync();
+            for (int j = lane; j < PPW * kn; j += 64) {
+                const int jq = j / kn, jk = j - jq * kn;
+                SampleDesc sd;
+                describe(p, s_lvl, t.n, t.m, t.q0 + jq, k0 + jk, true, sd);
+                s_off[wave][j] = sd.off;
+                s_w[wave][j] = sd.w;
+            }
+            wave_lds_sync();
+            if (active) {
+                const int base = ps * kn;
+#pragma unroll 4
+                for (int kk = 0; kk < kn; ++kk) {
+                    const int4 off = s_off[wave][base + kk];
+                    const float4 w = s_w[wave][base + kk];
+                    float v0[VEC], v1[VEC], v2[VEC], v3[VEC];
+                    Row<T, VEC>::load(v0, vr, ((uint32_t)off.x << Row<T, VEC>::kShift) + chan_bytes);
+                    Row<T, VEC>::load(v1, vr, ((uint32_t)off.y << Row<T, VEC>::kShift) + chan_bytes);
+                    Row<T, VEC>::load(v2, vr, ((uint32_t)off.z << Row<T, VEC>::kShift) + chan_bytes);
+                    Row<T, VEC>::load(v3, vr, ((uint32_t)off.w << Row<T, VEC>::kShift) + chan_bytes);
+#pragma unroll
+                    for (int i = 0; i < VEC; ++i)
+                        acc[i] += w.x * v0[i] + w.y * v1[i] + w.z * v2[i] + w.w * v3[i];
+                }
+            }
+        }
+        if (active && q_mine < p.Lq)
+            Row<T, VEC>::store(out + ((size_t)(t.n * p.Lq + q_mine) * p.M + t.m) * p.D + chan, acc);
+    }
+}
+
+// ---------------------------------------------------------------- backward
+
+template <typename T, int VEC, int LPP>
+__global__ __launch_bounds__(kBlock) void bwd_kernel(Params p) {
+    constexpr int PPW = 64 / LPP;
+    __shared__ int s_lvl[3 * kMaxLevels];
+    __shared__ int4 s_off[kWaves][kMaxItems];
+    __shared__ float4 s_w[kWaves][kMaxItems];
+    __shared__ float4 s_x[kWaves][kMaxItems];  // {a, lh, lw, -} in, {grad_attn, gx, gy, -} out
+    load_levels(p, s_lvl);
+
+    Tile t;
+    if (!tile_of(p, PPW, t)) return;
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    const int ps = lane / LPP, sub = lane % LPP;
+    const int K = p.K;
+    const int KC = K < kMaxItems / PPW ? K : kMaxItems / PPW;
+    const rsrc_t vr = make_rsrc(p.value, p.value_bytes);
+    const rsrc_t gr = make_rsrc(p.grad_value, p.gv_bytes);
+    const T* gout = static_cast<const T*>(p.grad_out);
+    const int q_mine = t.q0 + ps;
+    const bool q_ok = q_mine < p.Lq;
+    const size_t gout_row = ((size_t)(t.n * p.Lq + (q_ok ? q_mine : 0)) * p.M + t.m) * p.D;
+
+    for (int k0 = 0; k0 < K; k0 += KC) {
+        const int kn = K - k0 < KC ? K - k0 : KC;
+        wave_lds_sync();
+        for (int j = lane; j < PPW * kn; j += 64) {
+            const int jq = j / kn, jk = j - jq * kn;
+            SampleDesc sd;
+            describe(p, s_lvl, t.n, t.m, t.q0 + jq, k0 + jk, false, sd);
+            s_off[wave][j] = sd.off;
+            s_w[wave][j] = sd.w;
+            s_x[wave][j] = make_float4(sd.a, sd.lh, sd.lw, 0.f);
+        }
+        wave_lds_sync();
+        const int base = ps * kn;
+        for (int kk = 0; kk < kn; ++kk) {
+            const int4 off = s_off[wave][base + kk];
+            const float4 w = s_w[wave][base + kk];
+            const float4 x = s_x[wave][base + kk];
+            const float a = x.x, lh = x.y, lw = x.z, hh = 1.f - lh, hw = 1.f - lw;
+            float ga = 0.f, gw = 0.f, gh = 0.f;
+            for (int c0 = 0; c0 < p.D; c0 += LPP * VEC) {
+                const int chan = c0 + sub * VEC;
+                if (chan < p.D) {
+                    const uint32_t cb = (uint32_t)chan << Row<T, VEC>::kShift;
+                    float g[VEC], v0[VEC], v1[VEC], v2[VEC], v3[VEC];
+                    Row<T, VEC>::load_ptr(g, gout + gout_row + chan);
+                    Row<T, VEC>::load(v0, vr, ((uint32_t)off.x << Row<T, VEC>::kShift) + cb);
+                    Row<T, VEC>::load(v1, vr, ((uint32_t)off.y << Row<T, VEC>::kShift) + cb);
+                    Row<T, VEC>::load(v2, vr, ((uint32_t)off.z << Row<T, VEC>::kShift) + cb);
+                    Row<T, VEC>::load(v3, vr, ((uint32_t)off.w << Row<T, VEC>::kShift) + cb);
+#pragma unroll
+                    for (int i = 0; i < VEC; ++i) {
+                        const float s = w.x * v0[i] + w.y * v1[i] + w.z * v2[i] + w.w * v3[i];
+                        ga += g[i] * s;
+                        gw += g[i] * (hh * (v1[i] - v0[i]) + lh * (v3[i] - v2[i]));
+                        gh += g[i] * (hw * (v2[i] - v0[i]) + lw * (v3[i] - v1[i]));
+                    }
+                    // grad_value[corner] += a * w_corner * g   (fp32 rows)
+                    const uint32_t gcb = (uint32_t)chan << 2;
+                    const float a0 = a * w.x, a1 = a * w.y, a2 = a * w.z, a3 = a * w.w;
+#pragma unroll
+                    for (int i = 0; i < VEC; ++i) {
+                        const uint32_t ci = gcb + 4u * i;
+                        __builtin_amdgcn_raw_ptr_buffer_atomic_fadd_f32(a0 * g[i], gr, ((uint32_t)off.x << 2) + ci, 0, 0);
+                        __builtin_amdgcn_raw_ptr_buffer_atomic_fadd_f32(a1 * g[i], gr, ((uint32_t)off.y << 2) + ci, 0, 0);
+                        __builtin_amdgcn_raw_ptr_buffer_atomic_fadd_f32(a2 * g[i], gr, ((uint32_t)off.z << 2) + ci, 0, 0);
+                        __builtin_amdgcn_raw_ptr_buffer_atomic_fadd_f32(a3 * g[i], gr, ((uint32_t)off.w << 2) + ci, 0, 0);
+                    }
+                }
+            }
+            ga = group_sum<LPP>(ga);
+            gw = group_sum<LPP>(gw);
+            gh = group_sum<LPP>(gh);
+            if (sub == 0) {
+                const int l = (k0 + kk) / p.P;
+                const float Wf = (float)s_lvl[kMaxLevels + l], Hf = (float)s_lvl[l];
+                s_x[wave][base + kk] = make_float4(ga, Wf * (a * gw), Hf * (a * gh), 0.f);
+            }
+        }
+        wave_lds_sync();
+        for (int j = lane; j < PPW * kn; j += 64) {
+            const int jq = j / kn, jk = j - jq * kn;
+            const int q = t.q0 + jq;
+            if (q < p.Lq) {
+                const int smp = ((t.n * p.Lq + q) * p.M + t.m) * K + k0 + jk;
+                const float4 r = s_x[wave][j];
+                p.grad_attn[smp] = r.x;
+                reinterpret_cast<float2*>(p.grad_loc)[smp] = make_float2(r.y, r.z);
+            }
+        }
+    }
+}
+
+__global__ __launch_bounds__(256) void zero_kernel(float4* p, int64_t n4, float* tail, int ntail) {
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n4; i += stride)
+        p[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (blockIdx.x == 0 && (int)threadIdx.x < ntail) tail[threadIdx.x] = 0.f;
+}
+
+// ---------------------------------------------------------------- dispatch
+
+template <typename T>
+int pick_vec(int D) {
+    constexpr int kMax = 16 / sizeof(T);
+    for (int v = kMax; v > 1; v >>= 1)
+        if (D % v == 0) return v;
+    return 1;
+}
+
+int pick_lpp(int D, int vec) {
+    int need = (D + vec - 1) / vec;
+    int lpp = 1;
+    while (lpp < need && lpp < 64) lpp <<= 1;
+    return lpp;
+}
+
+template <template <typename, int, int> class KernelT, typename T, int VEC>
+hipError_t launch_lpp(Params p, int lpp, hipStream_t stream) {
+    auto go = [&](auto kernel, int ppw) -> hipError_t {
+        p.q_per_block = kWaves * ppw;
+        p.chunks = (p.Lq + p.q_per_block - 1) / p.q_per_block;
+        p.num_blocks = p.n_batch * p.M * p.chunks;
+        if (p.num_blocks == 0) return hipSuccess;
+        const int grid = (p.num_blocks + 7) / 8 * 8;
+        hipLaunchKernelGGL(kernel, dim3(grid), dim3(kBlock), 0, stream, p);
+        return hipGetLastError();
+    };
+    switch (lpp) {
+        case 1: return go(KernelT<T, VEC, 1>::fn(), 64);
+        case 2: return go(KernelT<T, VEC, 2>::fn(), 32);
+        case 4: return go(KernelT<T, VEC, 4>::fn(), 16);
+        case 8: return go(KernelT<T, VEC, 8>::fn(), 8);
+        case 16: return go(KernelT<T, VEC, 16>::fn(), 4);
+        case 32: return go(KernelT<T, VEC, 32>::fn(), 2);
+        default: return go(KernelT<T, VEC, 64>::fn(), 1);
+    }
+}
+
+template <typename T, int VEC, int LPP>
+struct FwdK {
+    static auto fn() { return fwd_kernel<T, VEC, LPP>; }
+};
+template <typename T, int VEC, int LPP>
+struct BwdK {
+    static auto fn() { return bwd_kernel<T, VEC, LPP>; }
+};
+
+template <template <typename, int, int> class KernelT, typename T>
+hipError_t launch_typed(const Params& p, hipStream_t stream) {
+    const int vec = pick_vec<T>(p.D);
+    const int lpp = pick_lpp(p.D, vec);
+    switch (vec) {
+        case 1: return launch_lpp<KernelT, T, 1>(p, lpp, stream);
+        case 2: return launch_lpp<KernelT, T, 2>(p, lpp, stream);
+        case 4: return launch_lpp<KernelT, T, 4>(p, lpp, stream);
+        default:
+            if constexpr (sizeof(T) == 2) return launch_lpp<KernelT, T, 8>(p, lpp, stream);
+            return hipErrorInvalidValue;
+    }
+}
+
+}  // namespace
+
+hipError_t launch_forward(const Params& p, msda_dtype_t dtype, hipStream_t stream) {
+    return dtype == MSDA_F16 ? launch_typed<FwdK, _Float16>(p, stream) : launch_typed<FwdK, float>(p, stream);
+}
+
+hipError_t launch_backward(const Params& p, msda_dtype_t dtype, hipStream_t stream) {
+    return dtype == MSDA_F16 ? launch_typed<BwdK, _Float16>(p, stream) : launch_typed<BwdK, float>(p, stream);
+}
+
+hipError_t launch_zero(float* ptr, int64_t n, hipStream_t stream) {
+    if (n <= 0) return hipSuccess;
+    const int64_t n4 = n / 4;
+    const int ntail = (int)(n - n4 * 4);
+    int64_t blocks = (n4 + 255) / 256;
+    if (blocks > 8192) blocks = 8192;
+    if (blocks < 1) blocks = 1;
+    hipLaunchKernelGGL(zero_kernel, dim3((unsigned)blocks), dim3(256), 0, stream,
+                       reinterpret_cast<float4*>(ptr), n4, ptr + n4 * 4, ntail);
+    return hipGetLastError();
+}
+
+}  // namespace msda

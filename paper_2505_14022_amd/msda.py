@@ -1,0 +1,179 @@
+"""ctypes binding of libmsda (argument marshalling only).
+
+The functions mirror the C ABI in ``include/msda.h`` and take torch tensors for device memory:
+every step of the computation runs in the library's HIP kernels. There is no fallback: if
+``libmsda.so`` has not been built, or the GPU is missing, the calls raise.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Sequence, Tuple
+
+import numpy as np
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "_lib", "libmsda.so")
+
+MSDA_SUCCESS = 0
+MSDA_ERROR_INVALID_VALUE = 1
+MSDA_ERROR_NOT_SUPPORTED = 2
+MSDA_ERROR_LAUNCH_FAILED = 3
+MSDA_F32 = 0
+MSDA_F16 = 1
+MSDA_MAX_LEVELS = 16
+
+EXPORTED = ["msda_check_args", "msda_forward", "msda_backward", "msda_status_string",
+            "msda_last_error", "msda_version"]
+
+
+class MsdaError(RuntimeError):
+    def __init__(self, status: int, where: str, detail: str):
+        self.status = status
+        super().__init__(f"{where}: {status_string(status)}: {detail}")
+
+
+_lib = None
+
+
+def lib():
+    """The loaded libmsda (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with `python -m paper_2505_14022_amd.build`")
+        L = ctypes.CDLL(LIB_PATH)
+        i64, vp, ip = ctypes.c_int64, ctypes.c_void_p, ctypes.POINTER(ctypes.c_int64)
+        L.msda_check_args.argtypes = [ip, ip] + [i64] * 7 + [ctypes.c_int]
+        L.msda_check_args.restype = ctypes.c_int
+        L.msda_forward.argtypes = [vp, ip, ip, vp, vp, vp] + [i64] * 7 + [ctypes.c_int, vp]
+        L.msda_forward.restype = ctypes.c_int
+        L.msda_backward.argtypes = [vp, ip, ip, vp, vp, vp, vp, vp, vp] + [i64] * 7 + [ctypes.c_int, vp]
+        L.msda_backward.restype = ctypes.c_int
+        L.msda_status_string.argtypes = [ctypes.c_int]
+        L.msda_status_string.restype = ctypes.c_char_p
+        L.msda_last_error.argtypes = []
+        L.msda_last_error.restype = ctypes.c_char_p
+        L.msda_version.argtypes = []
+        L.msda_version.restype = ctypes.c_int
+        _lib = L
+    return _lib
+
+
+def status_string(status: int) -> str:
+    return lib().msda_status_string(int(status)).decode()
+
+
+def last_error() -> str:
+    return lib().msda_last_error().decode()
+
+
+def _host_tables(spatial_shapes, level_start_index) -> Tuple[np.ndarray, np.ndarray]:
+    def to_np(x):
+        if hasattr(x, "detach"):
+            x = x.detach().cpu().numpy()
+        return np.ascontiguousarray(np.asarray(x), dtype=np.int64)
+
+    return to_np(spatial_shapes).reshape(-1), to_np(level_start_index).reshape(-1)
+
+
+def _iptr(a: np.ndarray):
+    return a.ctypes.data_as(ctypes.POINTER(ctypes.c_int64))
+
+
+def _dptr(t) -> Optional[int]:
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise ValueError("tensor arguments must be device tensors")
+    if not t.is_contiguous():
+        raise ValueError("tensor arguments must be contiguous")
+    return t.data_ptr()
+
+
+def _stream(stream) -> Optional[int]:
+    if stream is None:
+        import torch
+
+        return torch.cuda.current_stream().cuda_stream
+    return int(getattr(stream, "cuda_stream", stream))
+
+
+def _dtype_code(t) -> int:
+    import torch
+
+    if t.dtype == torch.float32:
+        return MSDA_F32
+    if t.dtype == torch.float16:
+        return MSDA_F16
+    raise ValueError(f"value dtype must be float32 or float16, got {t.dtype}")
+
+
+def _raise(st: int, where: str):
+    if st != MSDA_SUCCESS:
+        raise MsdaError(st, where, last_error())
+
+
+def check_args(spatial_shapes, level_start_index, N, S, M, D, Lq, L, P, dtype) -> int:
+    """msda_check_args: returns the status code (host-only, needs no GPU)."""
+    sh, st = _host_tables(spatial_shapes, level_start_index)
+    return lib().msda_check_args(_iptr(sh) if sh.size else None, _iptr(st) if st.size else None,
+                                 N, S, M, D, Lq, L, P, int(dtype))
+
+
+def _dims(value, sampling_loc):
+    N, S, M, D = value.shape
+    _, Lq, M2, L, P, two = sampling_loc.shape
+    if M2 != M or two != 2:
+        raise ValueError(f"sampling_loc shape {tuple(sampling_loc.shape)} does not match value {tuple(value.shape)}")
+    return N, S, M, D, Lq, L, P
+
+
+def forward(value, spatial_shapes, level_start_index, sampling_loc, attn_weight, out=None, stream=None):
+    """out[N, Lq, M*D] = MSDA(value, sampling_loc, attn_weight), computed by msda_forward."""
+    import torch
+
+    N, S, M, D, Lq, L, P = _dims(value, sampling_loc)
+    if out is None:
+        out = torch.empty((N, Lq, M * D), dtype=value.dtype, device=value.device)
+    sh, st = _host_tables(spatial_shapes, level_start_index)
+    r = lib().msda_forward(_dptr(value), _iptr(sh), _iptr(st), _dptr(sampling_loc), _dptr(attn_weight),
+                           _dptr(out), N, S, M, D, Lq, L, P, _dtype_code(value), _stream(stream))
+    _raise(r, "msda_forward")
+    return out
+
+
+def backward(value, spatial_shapes, level_start_index, sampling_loc, attn_weight, grad_out,
+             grad_value=None, grad_loc=None, grad_attn=None, stream=None):
+    """(grad_value fp32, grad_loc, grad_attn) from msda_backward."""
+    import torch
+
+    N, S, M, D, Lq, L, P = _dims(value, sampling_loc)
+    dev = value.device
+    if grad_value is None:
+        grad_value = torch.empty((N, S, M, D), dtype=torch.float32, device=dev)
+    if grad_loc is None:
+        grad_loc = torch.empty(tuple(sampling_loc.shape), dtype=torch.float32, device=dev)
+    if grad_attn is None:
+        grad_attn = torch.empty(tuple(attn_weight.shape), dtype=torch.float32, device=dev)
+    sh, st = _host_tables(spatial_shapes, level_start_index)
+    r = lib().msda_backward(_dptr(value), _iptr(sh), _iptr(st), _dptr(sampling_loc), _dptr(attn_weight),
+                            _dptr(grad_out), _dptr(grad_value), _dptr(grad_loc), _dptr(grad_attn),
+                            N, S, M, D, Lq, L, P, _dtype_code(value), _stream(stream))
+    _raise(r, "msda_backward")
+    return grad_value, grad_loc, grad_attn
+
+
+def forward_raw(value_ptr: int, shapes: np.ndarray, starts: np.ndarray, loc_ptr: int, attn_ptr: int,
+                out_ptr: int, dims: Sequence[int], dtype: int, stream: int) -> int:
+    """msda_forward on raw device addresses; returns the status (used by the benchmark loop)."""
+    return lib().msda_forward(value_ptr, _iptr(shapes), _iptr(starts), loc_ptr, attn_ptr, out_ptr,
+                              *dims, dtype, stream)
+
+
+def backward_raw(value_ptr: int, shapes: np.ndarray, starts: np.ndarray, loc_ptr: int, attn_ptr: int,
+                 gout_ptr: int, gv_ptr: int, gl_ptr: int, ga_ptr: int, dims: Sequence[int], dtype: int,
+                 stream: int) -> int:
+    """msda_backward on raw device addresses; returns the status (used by the benchmark loop)."""
+    return lib().msda_backward(value_ptr, _iptr(shapes), _iptr(starts), loc_ptr, attn_ptr, gout_ptr,
+                               gv_ptr, gl_ptr, ga_ptr, *dims, dtype, stream)

@@ -121,10 +121,12 @@ class Inputs:
     extra: dict = field(default_factory=dict)
 
 
-def _softmax_lastaxis(x: np.ndarray) -> np.ndarray:
-    x = x - x.max(axis=-1, keepdims=True)
-    e = np.exp(x)
-    return e / e.sum(axis=-1, keepdims=True)
+def _softmax_lastaxis_(x: np.ndarray) -> np.ndarray:
+    """In-place float32 softmax over the last axis."""
+    x -= x.max(axis=-1, keepdims=True)
+    np.exp(x, out=x)
+    x /= x.sum(axis=-1, keepdims=True)
+    return x
 
 
 def _own_pixel_refs(shapes) -> np.ndarray:
@@ -134,6 +136,16 @@ def _own_pixel_refs(shapes) -> np.ndarray:
         ys, xs = np.meshgrid((np.arange(h) + 0.5) / h, (np.arange(w) + 0.5) / w, indexing="ij")
         refs.append(np.stack([xs.ravel(), ys.ravel()], axis=-1))
     return np.concatenate(refs, axis=0)  # [S, 2] (x, y)
+
+
+def _to_f16(x: np.ndarray) -> np.ndarray:
+    """Round to fp16, nearest-even (torch's vectorized conversion; same bits as numpy's astype)."""
+    try:
+        import torch
+
+        return torch.from_numpy(np.ascontiguousarray(x)).half().numpy()
+    except ImportError:
+        return x.astype(np.float16)
 
 
 def generate(w: Workload, seed: Optional[int] = None) -> Inputs:
@@ -163,20 +175,31 @@ def generate(w: Workload, seed: Optional[int] = None) -> Inputs:
     if ref is None:
         loc = rng.uniform(w.ref_lo, w.ref_hi, size=(N, Lq, M, L, P, 2)).astype(np.float32)
     else:
-        off = rng.standard_normal((N, Lq, M, L, P, 2), dtype=np.float32) * np.float32(w.offset_px)
-        norm = np.asarray([[wl, hl] for hl, wl in w.shapes], dtype=np.float32)  # [L, 2] (W, H)
-        loc = (ref[:, :, None, None, None, :].astype(np.float32)
-               + off / norm[None, None, None, :, None, :]).astype(np.float32)
+        loc = rng.standard_normal((N, Lq, M, L, P, 2), dtype=np.float32)  # offsets, in pixels / offset_px
+        # normalized offset = offset_px * z / (W_l, H_l)
+        scale = np.asarray([[w.offset_px / wl, w.offset_px / hl] for hl, wl in w.shapes], dtype=np.float32)
+        loc *= scale[None, None, None, :, None, :]
+        loc += ref.astype(np.float32)[:, :, None, None, None, :]
 
     logits = rng.standard_normal((N, Lq, M, L * P), dtype=np.float32)
-    attn = _softmax_lastaxis(logits.astype(np.float64)).astype(np.float32).reshape(N, Lq, M, L, P)
+    attn = _softmax_lastaxis_(logits).reshape(N, Lq, M, L, P)
     grad_out = rng.standard_normal((N, Lq, M * D), dtype=np.float32)
 
     if w.dtype == "f16":
-        value = value.astype(np.float16)
-        grad_out = grad_out.astype(np.float16)
+        value = _to_f16(value)
+        grad_out = _to_f16(grad_out)
     elif w.dtype != "f32":
         raise ValueError(w.dtype)
     return Inputs(w=w, value=np.ascontiguousarray(value), shapes=shapes, starts=w.starts(),
                   loc=np.ascontiguousarray(loc), attn=np.ascontiguousarray(attn),
                   grad_out=np.ascontiguousarray(grad_out))
+
+
+def random_case(N: int, M: int, D: int, shapes, P: int, Lq: int, dtype: str = "f32", seed: int = 0,
+                lo: float = -0.1, hi: float = 1.1) -> Inputs:
+    """A generic random problem: value ~ N(0,1), locations ~ U(lo, hi) per coordinate (so a share
+    of samples falls off the map), softmax weights over L*P, grad_out ~ N(0,1)."""
+    shapes = tuple(tuple(int(v) for v in s) for s in shapes)
+    w = Workload(f"random_N{N}_M{M}_D{D}_L{len(shapes)}_P{P}_Lq{Lq}_{dtype}", N=N, M=M, D=D, shapes=shapes,
+                 P=P, Lq=Lq, dtype=dtype, refs="uniform_loc", offset_px=0.0, ref_lo=lo, ref_hi=hi)
+    return generate(w, seed=seed)

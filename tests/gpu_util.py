@@ -1,0 +1,108 @@
+"""Helpers for the GPU tests: run libmsda on seeded inputs and compare with the oracle."""
+from __future__ import annotations
+
+import sys
+from dataclasses import dataclass
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2505_14022_amd import msda, workloads
+
+# Tolerances: normwise per tensor, max_i |gpu_i - ref_i| / max_i |ref_i|.
+TOL_OUT_F32 = 1e-5
+TOL_OUT_F16 = 1e-3
+TOL_GRAD_VALUE = 1e-4
+TOL_GRAD_LOC = 1e-3
+TOL_GRAD_ATTN = 1e-3
+
+
+def say(msg: str):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def require_gpu():
+    import torch
+
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU visible")
+    msda.lib()  # raises if libmsda.so is missing: the GPU tests never fall back
+
+
+def normwise(gpu, ref) -> float:
+    gpu = np.asarray(gpu, dtype=np.float64)
+    ref = np.asarray(ref, dtype=np.float64)
+    if ref.size == 0:
+        return 0.0
+    scale = float(np.max(np.abs(ref)))
+    err = float(np.max(np.abs(gpu - ref)))
+    if scale == 0.0:
+        return err
+    return err / scale
+
+
+@dataclass
+class DeviceInputs:
+    value: "object"
+    loc: "object"
+    attn: "object"
+    grad_out: "object"
+
+
+def to_device(inp: workloads.Inputs) -> DeviceInputs:
+    import torch
+
+    dev = torch.device("cuda:0")
+    return DeviceInputs(value=torch.from_numpy(inp.value).to(dev), loc=torch.from_numpy(inp.loc).to(dev),
+                        attn=torch.from_numpy(inp.attn).to(dev), grad_out=torch.from_numpy(inp.grad_out).to(dev))
+
+
+def run_gpu(inp: workloads.Inputs, backward: bool = True):
+    import torch
+
+    d = to_device(inp)
+    out = msda.forward(d.value, inp.shapes, inp.starts, d.loc, d.attn)
+    res = {"out": out}
+    if backward:
+        gv, gl, ga = msda.backward(d.value, inp.shapes, inp.starts, d.loc, d.attn, d.grad_out)
+        res.update(grad_value=gv, grad_loc=gl, grad_attn=ga)
+    torch.cuda.synchronize()
+    return {k: v.float().cpu().numpy() if k != "out" else v.cpu().numpy() for k, v in res.items()}
+
+
+def run_oracle(inp: workloads.Inputs, backward: bool = True):
+    out = oracle.forward(inp.value, inp.shapes, inp.starts, inp.loc, inp.attn)
+    res = {"out": out}
+    if backward:
+        gv, gl, ga = oracle.backward(inp.value, inp.shapes, inp.starts, inp.loc, inp.attn, inp.grad_out)
+        res.update(grad_value=gv, grad_loc=gl, grad_attn=ga)
+    return res
+
+
+def check_parity(inp: workloads.Inputs, backward: bool = True, gpu=None, ref=None):
+    """Element-by-element comparison of every output; returns the error table."""
+    fp16 = inp.value.dtype == np.float16
+    gpu = gpu or run_gpu(inp, backward)
+    ref = ref or run_oracle(inp, backward)
+    errs = {"out": normwise(gpu["out"], ref["out"])}
+    tols = {"out": TOL_OUT_F16 if fp16 else TOL_OUT_F32}
+    if fp16:
+        # fp16 out: within one fp16 ulp of the exact (oracle) value, i.e. correctly rounded up to
+        # what fp32 accumulation can move (1e-6 of the largest output, which covers results too
+        # close to zero for fp16's grid to resolve the fp32 accumulation error)
+        r16 = np.abs(ref["out"]).astype(np.float16)
+        ulp = np.spacing(r16).astype(np.float64) + 1e-6 * float(np.max(np.abs(ref["out"])))
+        bad = np.abs(gpu["out"].astype(np.float64) - ref["out"]) > ulp
+        assert not bad.any(), f"{inp.w.name}: {int(bad.sum())} fp16 outputs more than 1 ulp from the oracle"
+    if backward:
+        for k, t in (("grad_value", TOL_GRAD_VALUE), ("grad_loc", TOL_GRAD_LOC), ("grad_attn", TOL_GRAD_ATTN)):
+            errs[k] = normwise(gpu[k], ref[k])
+            tols[k] = t
+    say(f"  {inp.w.name}: " + ", ".join(f"{k} {errs[k]:.2e} (tol {tols[k]:.0e})" for k in errs))
+    for k in errs:
+        assert gpu[k].shape == tuple(ref[k].shape), f"{k}: shape {gpu[k].shape} vs {ref[k].shape}"
+        assert np.all(np.isfinite(gpu[k])), f"{inp.w.name}: non-finite values in {k}"
+        assert errs[k] <= tols[k], f"{inp.w.name}: {k} normwise error {errs[k]:.3e} > {tols[k]:.0e}"
+    return errs

@@ -1,0 +1,153 @@
+"""The C ABI on the CPU: the library loads, exports what the header declares, and validates
+arguments before touching any device (no kernel is launched by these tests)."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+from paper_2505_14022_amd import msda, workloads
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "msda.h")
+
+
+def declared_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(msda_[a-z_]+)\s*\(", src)))
+
+
+@pytest.fixture(scope="module")
+def L():
+    if not os.path.exists(msda.LIB_PATH):
+        pytest.skip("libmsda.so not built")
+    return msda.lib()
+
+
+def test_header_declares_the_binding_surface():
+    assert declared_functions() == sorted(msda.EXPORTED)
+
+
+def test_library_exports_every_declared_symbol(L):
+    for name in declared_functions():
+        assert hasattr(L, name), f"{name} declared in include/msda.h but not exported"
+
+
+def test_status_strings_and_version(L):
+    assert msda.status_string(0) == "MSDA_SUCCESS"
+    assert msda.status_string(1) == "MSDA_ERROR_INVALID_VALUE"
+    assert msda.status_string(2) == "MSDA_ERROR_NOT_SUPPORTED"
+    assert msda.status_string(3) == "MSDA_ERROR_LAUNCH_FAILED"
+    assert msda.status_string(99) == "MSDA_UNKNOWN_STATUS"
+    assert L.msda_version() >= 100
+
+
+def _args(w):
+    return (w.shapes_array(), w.starts(), w.N, w.S, w.M, w.D, w.Lq, w.L, w.P,
+            msda.MSDA_F16 if w.dtype == "f16" else msda.MSDA_F32)
+
+
+@pytest.mark.parametrize("w", workloads.WORKLOADS, ids=lambda w: w.name)
+def test_every_workload_is_accepted(L, w):
+    assert msda.check_args(*_args(w)) == msda.MSDA_SUCCESS, msda.last_error()
+
+
+def test_bev_sca_listed_S_is_rejected(L):
+    # the BEVFormer spatial cross-attention shapes sum to 30825; a stated S of 30875 is inconsistent
+    w = workloads.BY_NAME["bev_sca"]
+    assert w.S == 30825
+    a = list(_args(w))
+    a[3] = 30875
+    assert msda.check_args(*a) == msda.MSDA_ERROR_INVALID_VALUE
+    assert "30825" in msda.last_error()
+
+
+def base():
+    shapes = np.asarray([[4, 6], [2, 3]], dtype=np.int64)
+    starts = np.asarray([0, 24], dtype=np.int64)
+    return [shapes, starts, 2, 30, 4, 8, 10, 2, 3, msda.MSDA_F32]
+
+
+@pytest.mark.parametrize("idx,val,status,needle", [
+    (2, -1, msda.MSDA_ERROR_INVALID_VALUE, "N="),
+    (6, -5, msda.MSDA_ERROR_INVALID_VALUE, "Lq="),
+    (4, 0, msda.MSDA_ERROR_INVALID_VALUE, "M="),
+    (5, 0, msda.MSDA_ERROR_INVALID_VALUE, "D="),
+    (8, 0, msda.MSDA_ERROR_INVALID_VALUE, "P="),
+    (3, 31, msda.MSDA_ERROR_INVALID_VALUE, "S=31"),
+    (9, 7, msda.MSDA_ERROR_INVALID_VALUE, "dtype"),
+    (5, 4097, msda.MSDA_ERROR_NOT_SUPPORTED, "4096"),
+])
+def test_check_args_rejects(L, idx, val, status, needle):
+    a = base()
+    assert msda.check_args(*a) == msda.MSDA_SUCCESS
+    a[idx] = val
+    assert msda.check_args(*a) == status
+    assert needle in msda.last_error()
+
+
+def test_check_args_level_table(L):
+    a = base()
+    a[1] = np.asarray([0, 23], dtype=np.int64)
+    assert msda.check_args(*a) == msda.MSDA_ERROR_INVALID_VALUE
+    assert "level_start_index[1]" in msda.last_error()
+    a = base()
+    a[0] = np.asarray([[4, 6], [0, 3]], dtype=np.int64)
+    assert msda.check_args(*a) == msda.MSDA_ERROR_INVALID_VALUE
+    a = base()
+    a[0] = np.ones((17, 2), dtype=np.int64)
+    a[1] = np.arange(17, dtype=np.int64)
+    a[3], a[7] = 17, 17
+    assert msda.check_args(*a) == msda.MSDA_ERROR_NOT_SUPPORTED
+    a = base()
+    assert L.msda_check_args(None, None, 2, 30, 4, 8, 10, 2, 3, 0) == msda.MSDA_ERROR_INVALID_VALUE
+
+
+def test_size_limit_is_reported(L):
+    # one batch item of 2^29 elements or more is beyond the per-launch index range
+    shapes = np.asarray([[1 << 14, 1 << 10]], dtype=np.int64)
+    a = [shapes, np.zeros(1, np.int64), 1, 1 << 24, 8, 4, 10, 1, 1, msda.MSDA_F32]
+    assert msda.check_args(*a) == msda.MSDA_ERROR_NOT_SUPPORTED
+    assert "limit" in msda.last_error()
+
+
+def _raw_forward(L, ptrs, a):
+    shapes, starts = a[0], a[1]
+    ip = ctypes.POINTER(ctypes.c_int64)
+    return L.msda_forward(*ptrs[:1], shapes.ctypes.data_as(ip), starts.ctypes.data_as(ip), *ptrs[1:],
+                          *a[2:9], a[9], None)
+
+
+def test_forward_checks_pointers_before_launching(L):
+    a = base()
+    # null device pointers with nonzero extent: rejected on the host
+    assert _raw_forward(L, [None, None, None, None], a) == msda.MSDA_ERROR_INVALID_VALUE
+    # misaligned value pointer: rejected on the host (the address is never dereferenced)
+    assert _raw_forward(L, [0x1004, 0x2000, 0x3000, 0x4000], a) == msda.MSDA_ERROR_INVALID_VALUE
+    assert "misaligned" in msda.last_error()
+    # a bad level table is reported before pointers are looked at
+    a[3] = 99
+    assert _raw_forward(L, [None, None, None, None], a) == msda.MSDA_ERROR_INVALID_VALUE
+    assert "S=99" in msda.last_error()
+
+
+def test_forward_empty_is_noop(L):
+    a = base()
+    a[2] = 0  # N = 0: nothing to do, no pointer is needed and nothing is launched
+    assert _raw_forward(L, [None, None, None, None], a) == msda.MSDA_SUCCESS
+    a = base()
+    a[6] = 0  # Lq = 0
+    assert _raw_forward(L, [None, None, None, None], a) == msda.MSDA_SUCCESS
+
+
+def test_backward_checks_pointers_before_launching(L):
+    a = base()
+    ip = ctypes.POINTER(ctypes.c_int64)
+    r = L.msda_backward(None, a[0].ctypes.data_as(ip), a[1].ctypes.data_as(ip), None, None, None, None, None,
+                        None, *a[2:9], a[9], None)
+    assert r == msda.MSDA_ERROR_INVALID_VALUE
+    r = L.msda_backward(0x1000, a[0].ctypes.data_as(ip), a[1].ctypes.data_as(ip), 0x2000, 0x3000, 0x4000,
+                        0x5008, 0x6000, 0x7000, *a[2:9], a[9], None)
+    assert r == msda.MSDA_ERROR_INVALID_VALUE and "grad_value" in msda.last_error()
