@@ -29,13 +29,15 @@
  *   grad_attn    [N, Lq, M, L, P]    fp32
  *
  * Ownership and execution. All tensor pointers are DEVICE pointers owned by the caller, except the
- * two level tables, which are HOST pointers read during the call. The library allocates no memory,
- * keeps no state between calls, never synchronizes and never prints. Work is enqueued on `stream`
- * (a hipStream_t; NULL means the default stream) and the call returns before it completes.
- * Outputs are overwritten entirely and must not alias inputs. Inputs are not modified.
+ * two level tables, which are HOST pointers read during the call. The library allocates no memory
+ * (the backward's scratch is a caller-provided workspace), keeps no state between calls, never
+ * synchronizes and never prints. Work is enqueued on `stream` (a hipStream_t; NULL means the
+ * default stream) and the call returns before it completes. Outputs are overwritten entirely and
+ * must not alias inputs or the workspace. Inputs are not modified.
  * Arithmetic is fp32 (fp16 inputs are converted exactly; fp16 out is rounded to nearest-even
- * once). grad_value is accumulated with fp32 atomics, so its low bits depend on the order in
- * which additions land.
+ * once). The order in which contributions to one grad_value element are summed depends on
+ * scheduling, so its low bits may differ between runs; out, grad_loc and grad_attn are
+ * reproducible bit for bit.
  *
  * Errors are returned, never raised: nothing is launched when a check fails, and
  * msda_last_error() then describes the failed check (thread-local, valid until the next call on
@@ -44,6 +46,7 @@
 #ifndef MSDA_H_
 #define MSDA_H_
 
+#include <stddef.h>
 #include <stdint.h>
 
 #ifdef __cplusplus
@@ -88,19 +91,36 @@ msda_status_t msda_forward(const void* value, const int64_t* spatial_shapes,
 
 /*
  * Backward pass (Sec. 4.2): given grad_out = dLoss/dout, write
- *   grad_value = dLoss/dvalue (zeroed, then accumulated by scatter-add),
- *   grad_loc   = dLoss/dsampling_loc, grad_attn = dLoss/dattn_weight.
+ *   grad_value = dLoss/dvalue, grad_loc = dLoss/dsampling_loc, grad_attn = dLoss/dattn_weight.
  * At an integer h_im (or w_im) the location gradient is the one of the cell [floor, floor+1];
  * samples outside the open range above get zero location and weight gradients.
+ *
+ * workspace: DEVICE scratch of at least the size msda_backward_workspace_size() reports, 256-byte
+ * aligned, owned by the caller and not used by anything else until the enqueued work completes.
+ * With a workspace, grad_value is computed owner-by-owner: samples are sorted by the pixel tile
+ * they touch and each grad_value row is written once by the wave that owns its tile. With
+ * workspace == NULL, grad_value is zeroed and accumulated with fp32 atomics (slower). A non-null
+ * workspace smaller than required is an error.
+ *
  * value and grad_out 16-byte aligned; grad_value 16-byte; grad_loc 8-byte; grad_attn 4-byte.
  * N*Lq == 0 still zeroes grad_value.
  */
 msda_status_t msda_backward(const void* value, const int64_t* spatial_shapes,
                             const int64_t* level_start_index, const float* sampling_loc,
                             const float* attn_weight, const void* grad_out, float* grad_value,
-                            float* grad_loc, float* grad_attn,
+                            float* grad_loc, float* grad_attn, void* workspace, size_t workspace_bytes,
                             int64_t N, int64_t S, int64_t M, int64_t D, int64_t Lq, int64_t L,
                             int64_t P, int dtype, void* stream);
+
+/*
+ * Workspace bytes msda_backward needs for this problem to take the owner-computes grad_value
+ * path (host-only; checks the problem like msda_check_args). *bytes is 0 when that path does not
+ * apply (D > 64, more than 16384 tile bins per (batch, head) slab, or an empty problem); then
+ * msda_backward ignores the workspace and uses atomics.
+ */
+msda_status_t msda_backward_workspace_size(const int64_t* spatial_shapes, const int64_t* level_start_index,
+                                           int64_t N, int64_t S, int64_t M, int64_t D, int64_t Lq,
+                                           int64_t L, int64_t P, int dtype, size_t* bytes);
 
 /* Static name of a status code ("MSDA_SUCCESS", ...). */
 const char* msda_status_string(msda_status_t status);

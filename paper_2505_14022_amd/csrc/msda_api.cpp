@@ -134,30 +134,64 @@ msda_status_t msda_forward(const void* value, const int64_t* spatial_shapes, con
     return ok();
 }
 
+msda_status_t msda_backward_workspace_size(const int64_t* spatial_shapes, const int64_t* level_start_index,
+                                           int64_t N, int64_t S, int64_t M, int64_t D, int64_t Lq, int64_t L,
+                                           int64_t P, int dtype, size_t* bytes) {
+    if (!bytes) return fail(MSDA_ERROR_INVALID_VALUE, "bytes must be non-null");
+    *bytes = 0;
+    msda_status_t st = check_problem(spatial_shapes, level_start_index, N, S, M, D, Lq, L, P, dtype);
+    if (st != MSDA_SUCCESS) return st;
+    if (N * Lq == 0) return ok();
+    const int64_t nb = batch_per_launch(S, M, D, Lq, L, P);
+    msda::Params p = base_params(spatial_shapes, level_start_index, S, M, D, Lq, L, P);
+    p.n_batch = (int)(N < nb ? N : nb);
+    if (msda::plan_binned(p)) *bytes = msda::binned_workspace_bytes(p);
+    return ok();
+}
+
 msda_status_t msda_backward(const void* value, const int64_t* spatial_shapes, const int64_t* level_start_index,
                             const float* sampling_loc, const float* attn_weight, const void* grad_out,
-                            float* grad_value, float* grad_loc, float* grad_attn, int64_t N, int64_t S, int64_t M,
-                            int64_t D, int64_t Lq, int64_t L, int64_t P, int dtype, void* stream) {
+                            float* grad_value, float* grad_loc, float* grad_attn, void* workspace,
+                            size_t workspace_bytes, int64_t N, int64_t S, int64_t M, int64_t D, int64_t Lq,
+                            int64_t L, int64_t P, int dtype, void* stream) {
     msda_status_t st = check_problem(spatial_shapes, level_start_index, N, S, M, D, Lq, L, P, dtype);
     if (st != MSDA_SUCCESS) return st;
     if (N == 0) return ok();
     if (!grad_value) return fail(MSDA_ERROR_INVALID_VALUE, "grad_value must be non-null");
     if (!aligned(grad_value, 16)) return fail(MSDA_ERROR_INVALID_VALUE, "misaligned grad_value: 16 bytes needed");
-    if (Lq > 0) {
-        if (!value || !sampling_loc || !attn_weight || !grad_out || !grad_loc || !grad_attn)
-            return fail(MSDA_ERROR_INVALID_VALUE,
-                        "value, sampling_loc, attn_weight, grad_out, grad_loc and grad_attn must be non-null");
-        if (!aligned(value, 16) || !aligned(grad_out, 16) || !aligned(sampling_loc, 8) || !aligned(grad_loc, 8) ||
-            !aligned(attn_weight, 4) || !aligned(grad_attn, 4))
-            return fail(MSDA_ERROR_INVALID_VALUE,
-                        "misaligned pointer: value and grad_out need 16 bytes, sampling_loc and grad_loc 8, "
-                        "attn_weight and grad_attn 4");
+    hipStream_t s = (hipStream_t)stream;
+    if (Lq == 0) {
+        hipError_t e = msda::launch_zero(grad_value, N * S * M * D, s);
+        if (e != hipSuccess) return fail(MSDA_ERROR_LAUNCH_FAILED, "grad_value zeroing: %s", hipGetErrorString(e));
+        return ok();
     }
-    hipError_t e = msda::launch_zero(grad_value, N * S * M * D, (hipStream_t)stream);
-    if (e != hipSuccess) return fail(MSDA_ERROR_LAUNCH_FAILED, "grad_value zeroing: %s", hipGetErrorString(e));
-    if (Lq == 0) return ok();
+    if (!value || !sampling_loc || !attn_weight || !grad_out || !grad_loc || !grad_attn)
+        return fail(MSDA_ERROR_INVALID_VALUE,
+                    "value, sampling_loc, attn_weight, grad_out, grad_loc and grad_attn must be non-null");
+    if (!aligned(value, 16) || !aligned(grad_out, 16) || !aligned(sampling_loc, 8) || !aligned(grad_loc, 8) ||
+        !aligned(attn_weight, 4) || !aligned(grad_attn, 4))
+        return fail(MSDA_ERROR_INVALID_VALUE,
+                    "misaligned pointer: value and grad_out need 16 bytes, sampling_loc and grad_loc 8, "
+                    "attn_weight and grad_attn 4");
     const int es = elem_size(dtype);
     const int64_t nb = batch_per_launch(S, M, D, Lq, L, P);
+    // binned (owner-computes) grad_value when a workspace is given and the problem fits it
+    bool binned = false;
+    if (workspace) {
+        size_t need = 0;
+        msda_backward_workspace_size(spatial_shapes, level_start_index, N, S, M, D, Lq, L, P, dtype, &need);
+        if (need > 0) {
+            if (workspace_bytes < need)
+                return fail(MSDA_ERROR_INVALID_VALUE, "workspace of %zu bytes is smaller than the %zu needed",
+                            workspace_bytes, need);
+            if (!aligned(workspace, 256)) return fail(MSDA_ERROR_INVALID_VALUE, "workspace must be 256-byte aligned");
+            binned = true;
+        }
+    }
+    if (!binned) {
+        hipError_t e = msda::launch_zero(grad_value, N * S * M * D, s);
+        if (e != hipSuccess) return fail(MSDA_ERROR_LAUNCH_FAILED, "grad_value zeroing: %s", hipGetErrorString(e));
+    }
     for (int64_t n0 = 0; n0 < N; n0 += nb) {
         const int64_t cnt = N - n0 < nb ? N - n0 : nb;
         msda::Params p = base_params(spatial_shapes, level_start_index, S, M, D, Lq, L, P);
@@ -171,8 +205,16 @@ msda_status_t msda_backward(const void* value, const int64_t* spatial_shapes, co
         p.grad_attn = grad_attn + n0 * Lq * M * L * P;
         p.value_bytes = (uint32_t)(cnt * S * M * D * es);
         p.gv_bytes = (uint32_t)(cnt * S * M * D * 4);
-        e = msda::launch_backward(p, (msda_dtype_t)dtype, (hipStream_t)stream);
+        hipError_t e = msda::launch_backward_grads(p, (msda_dtype_t)dtype, !binned, s);
         if (e != hipSuccess) return fail(MSDA_ERROR_LAUNCH_FAILED, "backward launch: %s", hipGetErrorString(e));
+        if (binned) {
+            if (!msda::plan_binned(p))
+                return fail(MSDA_ERROR_LAUNCH_FAILED, "internal: binned plan changed between batches");
+            msda::bind_workspace(p, workspace);
+            e = msda::launch_backward_value_binned(p, (msda_dtype_t)dtype, s);
+            if (e != hipSuccess)
+                return fail(MSDA_ERROR_LAUNCH_FAILED, "backward grad_value launch: %s", hipGetErrorString(e));
+        }
     }
     return ok();
 }

@@ -1,0 +1,148 @@
+// MSDA backward, part 1 (paper Sec. 4.2): gradients w.r.t. the sampling locations and the
+// attention weights, for gfx950 (CDNA4, wave64).
+//
+// Same mapping as the forward kernel (one (batch, head) slab and a run of queries per workgroup,
+// LPP lanes per query, per-sample descriptions parked in LDS). For each sample every lane forms
+// its channels' share of <g, s>, <g, ds/dw_im> and <g, ds/dh_im> from the four gathered corner
+// rows; the shares are summed over the query's lanes with DPP row operations and written
+// coalesced through LDS. The ATOMIC variant also scatters a * w_corner * g into grad_value with
+// fp32 buffer atomics (the path used when no workspace is given).
+#include "msda_device.hpp"
+
+namespace msda {
+namespace {
+
+template <typename T, int VEC, int LPP, bool ATOMIC>
+__global__ __launch_bounds__(kBlock) void bwd_kernel(Params p) {
+    constexpr int PPW = 64 / LPP;
+    __shared__ int s_lvl[3 * kMaxLevels];
+    __shared__ int4 s_off[kWaves][kMaxItems];
+    __shared__ float4 s_w[kWaves][kMaxItems];
+    __shared__ float4 s_x[kWaves][kMaxItems];  // {a, lh, lw, -} in, {grad_attn, gx, gy, -} out
+    load_levels(p, s_lvl);
+
+    Tile t;
+    if (!tile_of(p, PPW, t)) return;
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    const int ps = lane / LPP, sub = lane % LPP;
+    const int K = p.K;
+    const int KC = K < kMaxItems / PPW ? K : kMaxItems / PPW;
+    const rsrc_t vr = make_rsrc(p.value, p.value_bytes);
+    const rsrc_t gr = make_rsrc(p.grad_value, p.gv_bytes);
+    const T* gout = static_cast<const T*>(p.grad_out);
+    const int q_mine = t.q0 + ps;
+    const bool q_ok = q_mine < p.Lq;
+    const size_t gout_row = ((size_t)(t.n * p.Lq + (q_ok ? q_mine : 0)) * p.M + t.m) * p.D;
+
+    for (int k0 = 0; k0 < K; k0 += KC) {
+        const int kn = K - k0 < KC ? K - k0 : KC;
+        wave_lds_sync();
+        for (int j = lane; j < PPW * kn; j += 64) {
+            const int jq = j / kn, jk = j - jq * kn;
+            SampleDesc sd;
+            describe(p, s_lvl, t.n, t.m, t.q0 + jq, k0 + jk, false, sd);
+            s_off[wave][j] = sd.off;
+            s_w[wave][j] = sd.w;
+            s_x[wave][j] = make_float4(sd.a, sd.lh, sd.lw, 0.f);
+        }
+        wave_lds_sync();
+        const int base = ps * kn;
+        for (int kk = 0; kk < kn; ++kk) {
+            const int4 off = s_off[wave][base + kk];
+            const float4 w = s_w[wave][base + kk];
+            const float4 x = s_x[wave][base + kk];
+            const float a = x.x, lh = x.y, lw = x.z, hh = 1.f - lh, hw = 1.f - lw;
+            float ga = 0.f, gw = 0.f, gh = 0.f;
+            for (int c0 = 0; c0 < p.D; c0 += LPP * VEC) {
+                const int chan = c0 + sub * VEC;
+                if (chan < p.D) {
+                    const uint32_t cb = (uint32_t)chan << Row<T, VEC>::kShift;
+                    float g[VEC], v0[VEC], v1[VEC], v2[VEC], v3[VEC];
+                    Row<T, VEC>::load_ptr(g, gout + gout_row + chan);
+                    Row<T, VEC>::load(v0, vr, ((uint32_t)off.x << Row<T, VEC>::kShift) + cb);
+                    Row<T, VEC>::load(v1, vr, ((uint32_t)off.y << Row<T, VEC>::kShift) + cb);
+                    Row<T, VEC>::load(v2, vr, ((uint32_t)off.z << Row<T, VEC>::kShift) + cb);
+                    Row<T, VEC>::load(v3, vr, ((uint32_t)off.w << Row<T, VEC>::kShift) + cb);
+#pragma unroll
+                    for (int i = 0; i < VEC; ++i) {
+                        const float s = w.x * v0[i] + w.y * v1[i] + w.z * v2[i] + w.w * v3[i];
+                        ga += g[i] * s;
+                        gw += g[i] * (hh * (v1[i] - v0[i]) + lh * (v3[i] - v2[i]));
+                        gh += g[i] * (hw * (v2[i] - v0[i]) + lw * (v3[i] - v1[i]));
+                    }
+                    if constexpr (ATOMIC) {
+                        // grad_value[corner] += a * w_corner * g   (fp32 rows)
+                        const uint32_t gcb = (uint32_t)chan << 2;
+                        const float a0 = a * w.x, a1 = a * w.y, a2 = a * w.z, a3 = a * w.w;
+#pragma unroll
+                        for (int i = 0; i < VEC; ++i) {
+                            const uint32_t ci = gcb + 4u * i;
+                            __builtin_amdgcn_raw_ptr_buffer_atomic_fadd_f32(a0 * g[i], gr, ((uint32_t)off.x << 2) + ci, 0, 0);
+                            __builtin_amdgcn_raw_ptr_buffer_atomic_fadd_f32(a1 * g[i], gr, ((uint32_t)off.y << 2) + ci, 0, 0);
+                            __builtin_amdgcn_raw_ptr_buffer_atomic_fadd_f32(a2 * g[i], gr, ((uint32_t)off.z << 2) + ci, 0, 0);
+                            __builtin_amdgcn_raw_ptr_buffer_atomic_fadd_f32(a3 * g[i], gr, ((uint32_t)off.w << 2) + ci, 0, 0);
+                        }
+                    }
+                }
+            }
+            ga = group_sum<LPP>(ga);
+            gw = group_sum<LPP>(gw);
+            gh = group_sum<LPP>(gh);
+            if (sub == 0) {
+                const int l = (k0 + kk) / p.P;
+                const float Wf = (float)s_lvl[kMaxLevels + l], Hf = (float)s_lvl[l];
+                s_x[wave][base + kk] = make_float4(ga, Wf * (a * gw), Hf * (a * gh), 0.f);
+            }
+        }
+        wave_lds_sync();
+        for (int j = lane; j < PPW * kn; j += 64) {
+            const int jq = j / kn, jk = j - jq * kn;
+            const int q = t.q0 + jq;
+            if (q < p.Lq) {
+                const int smp = ((t.n * p.Lq + q) * p.M + t.m) * K + k0 + jk;
+                const float4 r = s_x[wave][j];
+                p.grad_attn[smp] = r.x;
+                reinterpret_cast<float2*>(p.grad_loc)[smp] = make_float2(r.y, r.z);
+            }
+        }
+    }
+}
+
+template <typename T, int VEC, int LPP>
+struct BwdK {
+    static auto fn() { return bwd_kernel<T, VEC, LPP, false>; }
+};
+template <typename T, int VEC, int LPP>
+struct BwdAtomicK {
+    static auto fn() { return bwd_kernel<T, VEC, LPP, true>; }
+};
+
+__global__ __launch_bounds__(256) void zero_kernel(float4* p, int64_t n4, float* tail, int ntail) {
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n4; i += stride)
+        p[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (blockIdx.x == 0 && (int)threadIdx.x < ntail) tail[threadIdx.x] = 0.f;
+}
+
+}  // namespace
+
+hipError_t launch_backward_grads(const Params& p, msda_dtype_t dtype, bool atomic_grad_value, hipStream_t stream) {
+    if (atomic_grad_value)
+        return dtype == MSDA_F16 ? launch_typed<BwdAtomicK, _Float16>(p, stream)
+                                 : launch_typed<BwdAtomicK, float>(p, stream);
+    return dtype == MSDA_F16 ? launch_typed<BwdK, _Float16>(p, stream) : launch_typed<BwdK, float>(p, stream);
+}
+
+hipError_t launch_zero(float* ptr, int64_t n, hipStream_t stream) {
+    if (n <= 0) return hipSuccess;
+    const int64_t n4 = n / 4;
+    const int ntail = (int)(n - n4 * 4);
+    int64_t blocks = (n4 + 255) / 256;
+    if (blocks > 8192) blocks = 8192;
+    if (blocks < 1) blocks = 1;
+    hipLaunchKernelGGL(zero_kernel, dim3((unsigned)blocks), dim3(256), 0, stream,
+                       reinterpret_cast<float4*>(ptr), n4, ptr + n4 * 4, ntail);
+    return hipGetLastError();
+}
+
+}  // namespace msda

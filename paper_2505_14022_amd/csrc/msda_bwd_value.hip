@@ -1,0 +1,622 @@
+// MSDA backward, part 2 (paper Sec. 4.2): grad_value, computed owner-by-owner for gfx950.
+//
+// The scatter-add is the backward's bottleneck (Sec. 3; Sec. 4.2 staggers it to ease write
+// contention). On gfx950 fp32 atomics retire at a fixed rate of about 20 G 64-byte requests/s
+// whatever the working set, and LDS fp32 atomics are slower still, so instead of scattering,
+// every grad_value row is owned by exactly one wave and written once with plain stores:
+//
+//   1. count:   each sample is binned by the tile of its top-left corner (tiles of 1x1..8x8 pixels
+//               per level, sized so a tile sees a few hundred samples) and by which neighbouring
+//               tiles its other corners reach (class: interior / right / right+down / down).
+//               Workgroups count in an LDS histogram and add their totals to the global counts.
+//   2. scan:    exclusive prefix sums over bins (record offsets) and over tiles (work items: a
+//               tile whose visible samples exceed one chunk is split into several items).
+//   3. scatter: each sample's index is written into its bin (LDS ranks + one global atomic per
+//               workgroup and bin).
+//   4. fold:    one wave per work item zeroes an LDS tile, folds a*w_corner*g of every visible
+//               sample (own bin plus the left / up / up-left neighbours' straddling classes)
+//               and stores the tile's grad_value rows; items of a split tile add theirs with
+//               atomics into rows that were zeroed before.
+#include "msda_device.hpp"
+
+namespace msda {
+namespace {
+
+constexpr int kGeo = 7;  // per-level table in LDS: H, W, log2 tile h, log2 tile w, tiles_x, tile_base, start
+constexpr int kAccWaves = 4;
+
+__device__ __forceinline__ void load_geo(const Params& p, int* s) {
+    if (threadIdx.x < kMaxLevels) {
+        const int l = threadIdx.x;
+        const bool in = l < p.L;
+        s[0 * kMaxLevels + l] = in ? p.H[l] : 1;
+        s[1 * kMaxLevels + l] = in ? p.W[l] : 1;
+        s[2 * kMaxLevels + l] = in ? p.tile_lh[l] : 0;
+        s[3 * kMaxLevels + l] = in ? p.tile_lw[l] : 0;
+        s[4 * kMaxLevels + l] = in ? p.tiles_x[l] : 1;
+        s[5 * kMaxLevels + l] = in ? p.tile_base[l] : 0x7fffffff;
+        s[6 * kMaxLevels + l] = in ? p.start[l] : 0;
+    }
+    __syncthreads();
+}
+
+// Bin of a sample within its slab (tile * 4 + class), or -1 if the sample is off the map.
+// Uses the same fp32 coordinates as every other kernel, so the bin agrees with the corners.
+__device__ __forceinline__ int sample_bin(const int* g, int l, float2 xy) {
+    const int H = g[l], W = g[kMaxLevels + l];
+    const float Hf = (float)H, Wf = (float)W;
+    const float w_im = __builtin_fmaf(xy.x, Wf, -0.5f);
+    const float h_im = __builtin_fmaf(xy.y, Hf, -0.5f);
+    if (!(h_im > -1.f && w_im > -1.f && h_im < Hf && w_im < Wf)) return -1;
+    const int h0 = (int)floorf(h_im), w0 = (int)floorf(w_im);
+    const int th = g[2 * kMaxLevels + l], tw = g[3 * kMaxLevels + l];
+    const int mh = (1 << th) - 1, mw = (1 << tw) - 1;
+    const int hc = h0 < 0 ? 0 : h0, wc = w0 < 0 ? 0 : w0;
+    const bool right = w0 >= 0 && (w0 & mw) == mw && w0 + 1 < W;
+    const bool down = h0 >= 0 && (h0 & mh) == mh && h0 + 1 < H;
+    const int cls = right ? (down ? 2 : 1) : (down ? 3 : 0);
+    const int tile = g[5 * kMaxLevels + l] + (hc >> th) * g[4 * kMaxLevels + l] + (wc >> tw);
+    return tile * 4 + cls;
+}
+
+__device__ __forceinline__ int level_of_tile(const int* g, int L, int tin) {
+    int l = 0;
+    for (int i = 1; i < L; ++i)
+        if (tin >= g[5 * kMaxLevels + i]) l = i;
+    return l;
+}
+
+// ---------------------------------------------------------------- 1. count
+
+__global__ __launch_bounds__(256) void bin_count_kernel(Params p) {
+    extern __shared__ int hist[];  // bins of this slab
+    __shared__ int s_geo[kGeo * kMaxLevels];
+    const int bps = p.tiles_per_slab * 4;
+    for (int i = threadIdx.x; i < bps; i += 256) hist[i] = 0;
+    load_geo(p, s_geo);
+    const int slab = blockIdx.x / p.chunks, chunk = blockIdx.x - slab * p.chunks;
+    const int n = slab / p.M, m = slab - n * p.M;
+    const int q0 = chunk * p.q_per_block;
+    const int nq = min(p.q_per_block, p.Lq - q0);
+    const int nsamp = nq * p.K;
+    const float2* loc = reinterpret_cast<const float2*>(p.loc);
+    for (int j = threadIdx.x; j < nsamp; j += 256) {
+        const int jq = j / p.K, k = j - jq * p.K;
+        const int smp = ((n * p.Lq + q0 + jq) * p.M + m) * p.K + k;
+        const int b = sample_bin(s_geo, k / p.P, loc[smp]);
+        if (b >= 0) atomicAdd(&hist[b], 1);
+    }
+    __syncthreads();
+    int* counts = p.counts + (size_t)slab * bps;
+    for (int i = threadIdx.x; i < bps; i += 256) {
+        const int c = hist[i];
+        if (c) atomicAdd(&counts[i], c);
+    }
+}
+
+// ---------------------------------------------------------------- 2. scan
+
+struct TileInfo {
+    int own0, own1;  // own bins [own0, own1)
+    int l0, l1;      // left neighbour classes right, right+down
+    int u0, u1;      // up neighbour classes right+down, down
+    int d0, d1;      // up-left neighbour class right+down
+};
+
+// Bin ranges visible to tile t (global tile index); empty ranges for missing neighbours.
+__device__ __forceinline__ TileInfo tile_info(const Params& p, const int* g, int t) {
+    const int tin = t % p.tiles_per_slab;
+    const int l = level_of_tile(g, p.L, tin);
+    const int rel = tin - g[5 * kMaxLevels + l];
+    const int tx_n = g[4 * kMaxLevels + l];
+    const int ty = rel / tx_n, tx = rel - ty * tx_n;
+    TileInfo ti;
+    ti.own0 = 4 * t;
+    ti.own1 = 4 * t + 4;
+    ti.l0 = ti.l1 = ti.u0 = ti.u1 = ti.d0 = ti.d1 = 0;
+    if (tx > 0) {
+        ti.l0 = 4 * (t - 1) + 1;
+        ti.l1 = 4 * (t - 1) + 3;
+    }
+    if (ty > 0) {
+        ti.u0 = 4 * (t - tx_n) + 2;
+        ti.u1 = 4 * (t - tx_n) + 4;
+    }
+    if (tx > 0 && ty > 0) {
+        ti.d0 = 4 * (t - tx_n - 1) + 2;
+        ti.d1 = 4 * (t - tx_n - 1) + 3;
+    }
+    return ti;
+}
+
+__device__ __forceinline__ int range_sum(const int* c, int a, int b) {
+    int s = 0;
+    for (int i = a; i < b; ++i) s += c[i];
+    return s;
+}
+
+// Per tile: own sample count and number of work items (>= 1 so that every tile is stored).
+__device__ __forceinline__ void tile_totals(const Params& p, const int* g, int t, int& own, int& items) {
+    const TileInfo ti = tile_info(p, g, t);
+    own = range_sum(p.counts, ti.own0, ti.own1);
+    const int vis = own + range_sum(p.counts, ti.l0, ti.l1) + range_sum(p.counts, ti.u0, ti.u1) +
+                    range_sum(p.counts, ti.d0, ti.d1);
+    items = vis > 0 ? (vis + kChunkRecords - 1) / kChunkRecords : 1;
+}
+
+// Exclusive block scan of two sequences (256 threads); returns the block totals.
+__device__ __forceinline__ int2 block_scan2(int a, int b, int& pa, int& pb, int* s) {
+    s[threadIdx.x] = a;
+    s[256 + threadIdx.x] = b;
+    __syncthreads();
+    for (int off = 1; off < 256; off <<= 1) {
+        const int va = threadIdx.x >= (unsigned)off ? s[threadIdx.x - off] : 0;
+        const int vb = threadIdx.x >= (unsigned)off ? s[256 + threadIdx.x - off] : 0;
+        __syncthreads();
+        s[threadIdx.x] += va;
+        s[256 + threadIdx.x] += vb;
+        __syncthreads();
+    }
+    const int2 tot = make_int2(s[255], s[511]);
+    pa = s[threadIdx.x] - a;
+    pb = s[256 + threadIdx.x] - b;
+    __syncthreads();
+    return tot;
+}
+
+constexpr int kTilesPerThread = kScanTiles / 256;
+
+__global__ __launch_bounds__(256) void scan_reduce_kernel(Params p) {
+    __shared__ int s_geo[kGeo * kMaxLevels];
+    __shared__ int s[512];
+    load_geo(p, s_geo);
+    int own_sum = 0, item_sum = 0;
+    const int t0 = blockIdx.x * kScanTiles + threadIdx.x * kTilesPerThread;
+    for (int i = 0; i < kTilesPerThread; ++i) {
+        const int t = t0 + i;
+        if (t >= p.n_tiles) break;
+        int own, items;
+        tile_totals(p, s_geo, t, own, items);
+        own_sum += own;
+        item_sum += items;
+    }
+    int pa, pb;
+    const int2 tot = block_scan2(own_sum, item_sum, pa, pb, s);
+    if (threadIdx.x == 0) {
+        p.block_sums[2 * blockIdx.x] = tot.x;
+        p.block_sums[2 * blockIdx.x + 1] = tot.y;
+    }
+}
+
+// One workgroup: exclusive scan of the per-block totals, in place.
+__global__ __launch_bounds__(256) void scan_blocks_kernel(Params p) {
+    __shared__ int s[512];
+    int carry_a = 0, carry_b = 0;
+    for (int base = 0; base < p.scan_blocks; base += 256) {
+        const int i = base + threadIdx.x;
+        const int a = i < p.scan_blocks ? p.block_sums[2 * i] : 0;
+        const int b = i < p.scan_blocks ? p.block_sums[2 * i + 1] : 0;
+        int pa, pb;
+        const int2 tot = block_scan2(a, b, pa, pb, s);
+        if (i < p.scan_blocks) {
+            p.block_sums[2 * i] = carry_a + pa;
+            p.block_sums[2 * i + 1] = carry_b + pb;
+        }
+        carry_a += tot.x;
+        carry_b += tot.y;
+    }
+}
+
+__global__ __launch_bounds__(256) void scan_apply_kernel(Params p) {
+    __shared__ int s_geo[kGeo * kMaxLevels];
+    __shared__ int s[512];
+    load_geo(p, s_geo);
+    int own[kTilesPerThread], items[kTilesPerThread];
+    int own_sum = 0, item_sum = 0;
+    const int t0 = blockIdx.x * kScanTiles + threadIdx.x * kTilesPerThread;
+    for (int i = 0; i < kTilesPerThread; ++i) {
+        const int t = t0 + i;
+        own[i] = items[i] = 0;
+        if (t < p.n_tiles) tile_totals(p, s_geo, t, own[i], items[i]);
+        own_sum += own[i];
+        item_sum += items[i];
+    }
+    int pa, pb;
+    block_scan2(own_sum, item_sum, pa, pb, s);
+    int rec = p.block_sums[2 * blockIdx.x] + pa;
+    int item = p.block_sums[2 * blockIdx.x + 1] + pb;
+    for (int i = 0; i < kTilesPerThread; ++i) {
+        const int t = t0 + i;
+        if (t >= p.n_tiles) break;
+        for (int c = 0; c < 4; ++c) {
+            p.offsets[4 * t + c] = rec;
+            p.cursor[4 * t + c] = rec;
+            rec += p.counts[4 * t + c];
+        }
+        p.tile_chunks[t] = item;
+        for (int c = 0; c < items[i] && item + c < p.max_items; ++c) p.items[item + c] = t;
+        item += items[i];
+        if (t == p.n_tiles - 1) {
+            p.offsets[4 * p.n_tiles] = rec;
+            p.tile_chunks[p.n_tiles] = item < p.max_items ? item : p.max_items;
+        }
+    }
+}
+
+// Rows of tiles that are folded by several work items start at zero (they are added to).
+__global__ __launch_bounds__(256) void zero_split_kernel(Params p) {
+    __shared__ int s_geo[kGeo * kMaxLevels];
+    load_geo(p, s_geo);
+    const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
+    const int lane = threadIdx.x & 63;
+    if (t >= p.n_tiles) return;
+    if (p.tile_chunks[t + 1] - p.tile_chunks[t] <= 1) return;
+    const int slab = t / p.tiles_per_slab, tin = t - slab * p.tiles_per_slab;
+    const int n = slab / p.M, m = slab - n * p.M;
+    const int l = level_of_tile(s_geo, p.L, tin);
+    const int H = s_geo[l], W = s_geo[kMaxLevels + l];
+    const int th = s_geo[2 * kMaxLevels + l], tw = s_geo[3 * kMaxLevels + l];
+    const int rel = tin - s_geo[5 * kMaxLevels + l], txn = s_geo[4 * kMaxLevels + l];
+    const int ty = rel / txn, tx = rel - ty * txn;
+    const int st = s_geo[6 * kMaxLevels + l];
+    const int npx = 1 << (th + tw);
+    for (int e = lane; e < npx * p.D; e += 64) {
+        const int px = e / p.D, ch = e - px * p.D;
+        const int h = (ty << th) + (px >> tw), w = (tx << tw) + (px & ((1 << tw) - 1));
+        if (h < H && w < W) p.grad_value[((size_t)(n * p.S + st + h * W + w) * p.M + m) * p.D + ch] = 0.f;
+    }
+}
+
+// ---------------------------------------------------------------- 3. scatter
+
+constexpr int kScatterRounds = kCountQueries / 256;
+
+__global__ __launch_bounds__(256) void bin_scatter_kernel(Params p) {
+    extern __shared__ int hist[];  // bins of this slab
+    __shared__ int s_geo[kGeo * kMaxLevels];
+    const int bps = p.tiles_per_slab * 4;
+    for (int i = threadIdx.x; i < bps; i += 256) hist[i] = 0;
+    load_geo(p, s_geo);
+    const int slab = blockIdx.x / p.chunks, chunk = blockIdx.x - slab * p.chunks;
+    const int n = slab / p.M, m = slab - n * p.M;
+    const int q0 = chunk * p.q_per_block;
+    const int nq = min(p.q_per_block, p.Lq - q0);
+    const int nsamp = nq * p.K;
+    const float2* loc = reinterpret_cast<const float2*>(p.loc);
+    int bins[kScatterRounds], ranks[kScatterRounds], smps[kScatterRounds];
+#pragma unroll
+    for (int r = 0; r < kScatterRounds; ++r) {
+        const int j = threadIdx.x + 256 * r;
+        bins[r] = -1;
+        ranks[r] = 0;
+        smps[r] = 0;
+        if (j < nsamp) {
+            const int jq = j / p.K, k = j - jq * p.K;
+            const int smp = ((n * p.Lq + q0 + jq) * p.M + m) * p.K + k;
+            const int b = sample_bin(s_geo, k / p.P, loc[smp]);
+            smps[r] = smp;
+            bins[r] = b;
+            if (b >= 0) ranks[r] = atomicAdd(&hist[b], 1);
+        }
+    }
+    __syncthreads();
+    int* cursor = p.cursor + (size_t)slab * bps;
+    for (int i = threadIdx.x; i < bps; i += 256) {
+        const int c = hist[i];
+        if (c) hist[i] = atomicAdd(&cursor[i], c);
+    }
+    __syncthreads();
+#pragma unroll
+    for (int r = 0; r < kScatterRounds; ++r) {
+        if (bins[r] < 0) continue;
+        const int pos = hist[bins[r]] + ranks[r];
+        if (pos < p.n_samples) p.records[pos] = smps[r];  // always true when counts and cursor agree
+    }
+}
+
+// ---------------------------------------------------------------- 4. fold
+
+__device__ __forceinline__ int lane_i(int v, int r) { return __builtin_amdgcn_readlane(v, r); }
+__device__ __forceinline__ float lane_f(float v, int r) {
+    return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), r));
+}
+
+constexpr int kFoldBatch = 64;  // records described by one wave at a time (one per lane)
+
+// One wave per work item. A batch of up to 64 records is described one record per lane
+// (coordinates, tile-relative top-left corner, a * bilinear weights, grad_out row); then, per
+// block of 32 channels, every lane loads its channel of all 64 grad_out rows at once (64
+// independent loads in flight) and the records are folded in order: lanes 0-31 add the top two
+// corners, lanes 32-63 the bottom two, into the LDS tile with plain read-modify-writes (the wave
+// owns the tile, so no two lanes or records race).
+// DC: the channel count as a compile-time constant (0 = take it from p.D). With DC = 32 the two
+// corners of a row, 32 floats apart in LDS, are read and written as one ds_read2 / ds_write2.
+template <typename T, int DC>
+__global__ __launch_bounds__(256) void fold_kernel(Params p, int tile_floats) {
+    extern __shared__ float s_acc_all[];
+    __shared__ int s_geo[kGeo * kMaxLevels];
+    load_geo(p, s_geo);
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    float* acc = s_acc_all + wave * tile_floats;
+    const int total = p.tile_chunks[p.n_tiles];
+    const int nwaves = gridDim.x * kAccWaves;
+    const T* gout = static_cast<const T*>(p.grad_out);
+    const float2* loc = reinterpret_cast<const float2*>(p.loc);
+    const int half = lane >> 5, slot = lane & 31;
+    const int D = DC > 0 ? DC : p.D;
+
+    for (int item = blockIdx.x * kAccWaves + wave; item < total; item += nwaves) {
+        const int t = __builtin_amdgcn_readfirstlane(p.items[item]);
+        if (t < 0 || t >= p.n_tiles) continue;  // never taken: items holds tile indices
+        const int first = __builtin_amdgcn_readfirstlane(p.tile_chunks[t]);
+        const int nitems = __builtin_amdgcn_readfirstlane(p.tile_chunks[t + 1]) - first;
+        const int chunk = item - first;
+        const int slab = t / p.tiles_per_slab, tin = t - slab * p.tiles_per_slab;
+        const int n = slab / p.M, m = slab - n * p.M;
+        // the tile's geometry is the same for the whole wave: keep it in scalar registers
+        const int l = __builtin_amdgcn_readfirstlane(level_of_tile(s_geo, p.L, tin));
+        const int H = __builtin_amdgcn_readfirstlane(s_geo[l]);
+        const int W = __builtin_amdgcn_readfirstlane(s_geo[kMaxLevels + l]);
+        const int th = __builtin_amdgcn_readfirstlane(s_geo[2 * kMaxLevels + l]);
+        const int tw = __builtin_amdgcn_readfirstlane(s_geo[3 * kMaxLevels + l]);
+        const int TH = 1 << th, TW = 1 << tw;
+        const int rel = tin - __builtin_amdgcn_readfirstlane(s_geo[5 * kMaxLevels + l]);
+        const int txn = __builtin_amdgcn_readfirstlane(s_geo[4 * kMaxLevels + l]);
+        const int ty = rel / txn, tx = rel - ty * txn;
+        const int h_org = ty << th, w_org = tx << tw;
+        const int st = __builtin_amdgcn_readfirstlane(s_geo[6 * kMaxLevels + l]);
+        const float Hf = (float)H, Wf = (float)W;
+        const TileInfo ti = tile_info(p, s_geo, t);
+        const int a0 = p.offsets[ti.own0], a1 = p.offsets[ti.own1];
+        const int b0 = ti.l1 > ti.l0 ? p.offsets[ti.l0] : 0, b1 = ti.l1 > ti.l0 ? p.offsets[ti.l1] : 0;
+        const int c0 = ti.u1 > ti.u0 ? p.offsets[ti.u0] : 0, c1 = ti.u1 > ti.u0 ? p.offsets[ti.u1] : 0;
+        const int d0 = ti.d1 > ti.d0 ? p.offsets[ti.d0] : 0, d1 = ti.d1 > ti.d0 ? p.offsets[ti.d1] : 0;
+        const int na = __builtin_amdgcn_readfirstlane(a1 - a0), nb = __builtin_amdgcn_readfirstlane(b1 - b0);
+        const int nc = __builtin_amdgcn_readfirstlane(c1 - c0), nd = __builtin_amdgcn_readfirstlane(d1 - d0);
+        const int nvis = na + nb + nc + nd;
+        const int beg = __builtin_amdgcn_readfirstlane(chunk * kChunkRecords);
+        const int end = __builtin_amdgcn_readfirstlane(min(beg + kChunkRecords, nvis));
+
+        // the LDS tile carries a one-pixel margin on every side, so every corner of every visible
+        // record lands inside it; corners that are not on this tile fall in the margin (or in
+        // cells past the map edge) and are never stored
+        const int PW = TW + 2;
+        const int npad = (TH + 2) * PW;
+        for (int e = lane; e < npad * D; e += 64) acc[e] = 0.f;
+
+        for (int pos0 = beg; pos0 < end; pos0 += kFoldBatch) {
+            const int cnt = __builtin_amdgcn_readfirstlane(min(kFoldBatch, end - pos0));
+            // ---- describe one record per lane
+            int grow = 0, pk = 0, prow = -8, pcol = -8;
+            float w00 = 0.f, w01 = 0.f, w10 = 0.f, w11 = 0.f;
+            if (lane < cnt) {
+                int pos = pos0 + lane, idx;
+                if (pos < na) idx = a0 + pos;
+                else if ((pos -= na) < nb) idx = b0 + pos;
+                else if ((pos -= nb) < nc) idx = c0 + pos;
+                else idx = d0 + (pos - nc);
+                int smp = p.records[idx < p.n_samples ? idx : 0];
+                smp = smp < 0 || smp >= p.n_samples ? 0 : smp;  // never taken: every slot is filled
+                const int pair = smp / p.K;
+                const float2 xy = loc[smp];
+                const float a = p.attn[smp];
+                const float w_im = __builtin_fmaf(xy.x, Wf, -0.5f);
+                const float h_im = __builtin_fmaf(xy.y, Hf, -0.5f);
+                const float h0f = floorf(h_im), w0f = floorf(w_im);
+                const float lh = h_im - h0f, lw = w_im - w0f;
+                const float hh = 1.f - lh, hw = 1.f - lw;
+                // padded-tile coordinates of the top-left corner, both in [0, T]
+                prow = (int)h0f - h_org + 1;
+                pcol = (int)w0f - w_org + 1;
+                grow = pair * D;
+                pk = prow * PW + pcol;
+                w00 = a * (hh * hw);
+                w01 = a * (hh * lw);
+                w10 = a * (lh * hw);
+                w11 = a * (lh * lw);
+            }
+            // bit r: the 2x2 footprints of records r and r+1 do not overlap, so both can be
+            // read before either is written back
+            const int nrow = __shfl_down(prow, 1, 64), ncol = __shfl_down(pcol, 1, 64);
+            const int dr = prow - nrow, dc = pcol - ncol;
+            const uint64_t apart = __ballot(dr > 1 || dr < -1 || dc > 1 || dc < -1);
+            for (int ch0 = 0; ch0 < D; ch0 += 32) {
+                const int ch = ch0 + slot;
+                const bool ch_ok = ch < D;
+                const int chl = ch_ok ? ch : D - 1;  // keeps idle lanes inside the row and the tile
+                float gr[kFoldBatch];
+#pragma unroll
+                for (int r = 0; r < kFoldBatch; ++r) gr[r] = ch_ok ? (float)gout[lane_i(grow, r) + chl] : 0.f;
+                // lanes 0-31 fold the record's top row, lanes 32-63 its bottom row; lanes past D
+                // stay idle (they must not write: they would race with the lane owning D-1)
+                float* lane_acc = acc + chl + half * PW * D;
+                if (!ch_ok) continue;
+#pragma unroll
+                for (int r = 0; r < kFoldBatch; r += 2) {
+                    if (r >= cnt) continue;
+                    float* da = lane_acc + lane_i(pk, r) * D;
+                    const float a00 = lane_f(w00, r), a01 = lane_f(w01, r);
+                    const float a10 = lane_f(w10, r), a11 = lane_f(w11, r);
+                    const float wla = half ? a10 : a00, wra = half ? a11 : a01;
+                    if (r + 1 < cnt) {
+                        float* db = lane_acc + lane_i(pk, r + 1) * D;
+                        const float b00 = lane_f(w00, r + 1), b01 = lane_f(w01, r + 1);
+                        const float b10 = lane_f(w10, r + 1), b11 = lane_f(w11, r + 1);
+                        const float wlb = half ? b10 : b00, wrb = half ? b11 : b01;
+                        if ((apart >> r) & 1) {
+                            const float a0v = da[0], a1v = da[D], b0v = db[0], b1v = db[D];
+                            da[0] = a0v + wla * gr[r];
+                            da[D] = a1v + wra * gr[r];
+                            db[0] = b0v + wlb * gr[r + 1];
+                            db[D] = b1v + wrb * gr[r + 1];
+                        } else {
+                            da[0] += wla * gr[r];
+                            da[D] += wra * gr[r];
+                            db[0] += wlb * gr[r + 1];
+                            db[D] += wrb * gr[r + 1];
+                        }
+                    } else {
+                        da[0] += wla * gr[r];
+                        da[D] += wra * gr[r];
+                    }
+                }
+            }
+        }
+        wave_lds_sync();
+        const bool split = nitems > 1;
+        const int npx = TH * TW;
+        for (int e = lane; e < npx * D; e += 64) {
+            const int px = e / D, ch = e - px * D;
+            const int pr = px >> tw, pc = px & (TW - 1);
+            const int h = h_org + pr, w = w_org + pc;
+            if (h < H && w < W) {
+                const float v = acc[((pr + 1) * PW + pc + 1) * D + ch];
+                float* dst = p.grad_value + ((size_t)(n * p.S + st + h * W + w) * p.M + m) * D + ch;
+                if (split) unsafeAtomicAdd(dst, v);
+                else *dst = v;
+            }
+        }
+        wave_lds_sync();
+    }
+}
+
+}  // namespace
+
+// ---------------------------------------------------------------- host side
+
+bool plan_binned(Params& p) {
+    if (p.D > kBinnedMaxD || p.Lq == 0 || p.K > kCountQueries) return false;
+    // largest square tile (2^e x 2^e pixels) whose accumulator, with its one-pixel margin, fits
+    auto padded = [&](int eh, int ew) { return ((1 << eh) + 2) * ((1 << ew) + 2) * p.D; };
+    if (padded(0, 0) > kTileFloats) return false;
+    int e_max = 0;
+    while (e_max < 3 && padded(e_max + 1, e_max + 1) <= kTileFloats) ++e_max;
+    int lh[kMaxLevels], lw[kMaxLevels];
+    for (int l = 0; l < p.L; ++l) {
+        // corner hits per pixel of one (n, m) slab if locations were spread evenly; a sample is
+        // recorded once (in the tile of its top-left corner), so records per pixel ~ hits / 4
+        // plus the ~25% that straddle into neighbours
+        const double hits = 4.0 * p.Lq * p.P / ((double)p.H[l] * p.W[l]);
+        const double rec_px = hits * 0.32 + 1e-9;
+        const double target_px = (kChunkRecords / 2) / rec_px;
+        int e = (int)floor(log(target_px) / log(4.0) + 0.5);  // square tiles of 4^e pixels
+        if (e < 0) e = 0;
+        if (e > e_max) e = e_max;
+        lh[l] = lw[l] = e;
+    }
+    auto tiles_of = [&](int l) {
+        const int th = 1 << lh[l], tw = 1 << lw[l];
+        return (int64_t)((p.H[l] + th - 1) / th) * ((p.W[l] + tw - 1) / tw);
+    };
+    for (;;) {
+        int64_t tps = 0;
+        for (int l = 0; l < p.L; ++l) tps += tiles_of(l);
+        if (tps * 4 <= kHistMax) break;
+        // coarsen the level with the most tiles that can still grow
+        int best = -1;
+        int64_t most = 0;
+        for (int l = 0; l < p.L; ++l)
+            if (padded(lh[l] + (lh[l] <= lw[l]), lw[l] + (lh[l] > lw[l])) <= kTileFloats && tiles_of(l) > most) {
+                most = tiles_of(l);
+                best = l;
+            }
+        if (best < 0) return false;
+        if (lh[best] <= lw[best]) ++lh[best];
+        else ++lw[best];
+    }
+    int base = 0;
+    for (int l = 0; l < kMaxLevels; ++l) {
+        if (l < p.L) {
+            p.tile_lh[l] = lh[l];
+            p.tile_lw[l] = lw[l];
+            p.tiles_x[l] = (p.W[l] + (1 << lw[l]) - 1) >> lw[l];
+            p.tile_base[l] = base;
+            base += (int)tiles_of(l);
+        } else {
+            p.tile_lh[l] = p.tile_lw[l] = 0;
+            p.tiles_x[l] = 1;
+            p.tile_base[l] = base;
+        }
+    }
+    p.tiles_per_slab = base;
+    const int64_t n_slabs = (int64_t)p.n_batch * p.M;
+    const int64_t n_tiles = n_slabs * base;
+    const int64_t n_samples = (int64_t)p.n_batch * p.Lq * p.M * p.K;
+    const int64_t max_items = 2 * n_tiles + 4 * n_samples / kChunkRecords + 1;
+    if (n_tiles * 4 + 1 > kMaxIndex || max_items > kMaxIndex || n_samples > kMaxIndex) return false;
+    p.n_slabs = (int)n_slabs;
+    p.n_tiles = (int)n_tiles;
+    p.n_samples = (int)n_samples;
+    p.max_items = (int)max_items;
+    p.scan_blocks = (int)((n_tiles + kScanTiles - 1) / kScanTiles);
+    return true;
+}
+
+namespace {
+size_t align256(size_t x) { return (x + 255) / 256 * 256; }
+}  // namespace
+
+size_t binned_workspace_bytes(const Params& p) {
+    const size_t nb = (size_t)p.n_tiles * 4;
+    return align256(nb * 4) + align256((nb + 1) * 4) + align256(nb * 4) + align256(((size_t)p.n_tiles + 1) * 4) +
+           align256((size_t)p.max_items * 4) + align256((size_t)p.scan_blocks * 2 * 4) +
+           align256((size_t)p.n_samples * 4);
+}
+
+void bind_workspace(Params& p, void* ws) {
+    char* c = static_cast<char*>(ws);
+    const size_t nb = (size_t)p.n_tiles * 4;
+    p.counts = reinterpret_cast<int*>(c);
+    c += align256(nb * 4);
+    p.offsets = reinterpret_cast<int*>(c);
+    c += align256((nb + 1) * 4);
+    p.cursor = reinterpret_cast<int*>(c);
+    c += align256(nb * 4);
+    p.tile_chunks = reinterpret_cast<int*>(c);
+    c += align256(((size_t)p.n_tiles + 1) * 4);
+    p.items = reinterpret_cast<int*>(c);
+    c += align256((size_t)p.max_items * 4);
+    p.block_sums = reinterpret_cast<int*>(c);
+    c += align256((size_t)p.scan_blocks * 2 * 4);
+    p.records = reinterpret_cast<int*>(c);
+}
+
+hipError_t launch_backward_value_binned(const Params& p0, msda_dtype_t dtype, hipStream_t stream) {
+    Params p = p0;
+    hipError_t e = launch_zero(reinterpret_cast<float*>(p.counts), (int64_t)p.n_tiles * 4, stream);
+    if (e != hipSuccess) return e;
+    p.q_per_block = kCountQueries / p.K > 0 ? kCountQueries / p.K : 1;
+    p.chunks = (p.Lq + p.q_per_block - 1) / p.q_per_block;
+    const int bin_blocks = p.n_slabs * p.chunks;
+    const size_t hist_lds = (size_t)p.tiles_per_slab * 4 * sizeof(int);
+    hipLaunchKernelGGL(bin_count_kernel, dim3(bin_blocks), dim3(256), hist_lds, stream, p);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    hipLaunchKernelGGL(scan_reduce_kernel, dim3(p.scan_blocks), dim3(256), 0, stream, p);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    hipLaunchKernelGGL(scan_blocks_kernel, dim3(1), dim3(256), 0, stream, p);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    hipLaunchKernelGGL(scan_apply_kernel, dim3(p.scan_blocks), dim3(256), 0, stream, p);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    hipLaunchKernelGGL(zero_split_kernel, dim3((p.n_tiles + 3) / 4), dim3(256), 0, stream, p);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    hipLaunchKernelGGL(bin_scatter_kernel, dim3(bin_blocks), dim3(256), hist_lds, stream, p);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    int tile_floats = 0;
+    for (int l = 0; l < p.L; ++l) {
+        const int f = ((1 << p.tile_lh[l]) + 2) * ((1 << p.tile_lw[l]) + 2) * p.D;
+        if (f > tile_floats) tile_floats = f;
+    }
+    const size_t lds = (size_t)kAccWaves * tile_floats * sizeof(float);
+    const int fold_blocks = 768;  // three workgroups per CU are resident (LDS-bound)
+    const bool d32 = p.D == 32;
+    if (dtype == MSDA_F16) {
+        if (d32) hipLaunchKernelGGL((fold_kernel<_Float16, 32>), dim3(fold_blocks), dim3(256), lds, stream, p, tile_floats);
+        else hipLaunchKernelGGL((fold_kernel<_Float16, 0>), dim3(fold_blocks), dim3(256), lds, stream, p, tile_floats);
+    } else {
+        if (d32) hipLaunchKernelGGL((fold_kernel<float, 32>), dim3(fold_blocks), dim3(256), lds, stream, p, tile_floats);
+        else hipLaunchKernelGGL((fold_kernel<float, 0>), dim3(fold_blocks), dim3(256), lds, stream, p, tile_floats);
+    }
+    return hipGetLastError();
+}
+
+}  // namespace msda

@@ -1,24 +1,8 @@
-// MSDA forward and backward kernels for gfx950 (CDNA4, wave64).
-//
-// The operation is the one of the paper's Sec. 3-4: per (query, head) pair, L*P bilinear samples
-// of the value tensor, weighted by attention weights and summed (forward); the gradients w.r.t.
-// locations, weights (reductions over channels) and value (scatter-add) (backward, Sec. 4.2).
-//
-// Mapping (shared by both passes):
-//   * A workgroup of 256 lanes owns one (batch n, head m) pair and a run of consecutive queries,
-//     so every value / grad_value row it touches lies in that head's slab. Workgroups are
-//     renumbered so that all the work of one (n, m) slab lands on one XCD (consecutive workgroup
-//     ids are dealt round-robin to the 8 XCDs): the slab's value lines stay in one XCD's L2 and
-//     grad_value atomics on a line come from one L2.
-//   * Within a wave, LPP lanes serve one query; each lane owns VEC contiguous channels, so one
-//     corner of one sample is a single coalesced row read (D=32 fp32: 8 lanes x 16 B = 128 B).
-//     A wave serves 64/LPP queries at once.
-//   * Phase 1: the wave computes the per-sample work (coordinates, range test, floor, the four
-//     corner rows and bilinear weights) once per sample, one sample per lane, and parks it in
-//     LDS. Phase 2: every lane of a query walks that query's samples, reading the parked
-//     description with a broadcast LDS read and gathering the four corner rows.
-//   * Off-map corners carry an out-of-range buffer offset: the buffer load returns zero and the
-//     buffer atomic is dropped by the hardware, with no branch.
+// Device-side helpers shared by the MSDA kernels (gfx950, wave64): buffer resources, row
+// loads / stores, lane-group reductions, the workgroup -> (batch, head, queries) mapping and the
+// per-sample description (Sec. 3: coordinates and the 2x2 bilinear neighbourhood).
+#pragma once
+
 #include <hip/hip_runtime.h>
 
 #include "msda_internal.h"
@@ -249,187 +233,26 @@ __device__ __forceinline__ void load_levels(const Params& p, int* s_lvl) {
     __syncthreads();
 }
 
-// ---------------------------------------------------------------- forward
+// ---------------------------------------------------------------- launch helpers
 
-template <typename T, int VEC, int LPP>
-__global__ __launch_bounds__(kBlock) void fwd_kernel(Params p) {
-    constexpr int PPW = 64 / LPP;
-    __shared__ int s_lvl[3 * kMaxLevels];
-    __shared__ int4 s_off[kWaves][kMaxItems];
-    __shared__ float4 s_w[kWaves][kMaxItems];
-    load_levels(p, s_lvl);
-
-    Tile t;
-    if (!tile_of(p, PPW, t)) return;
-    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-    const int ps = lane / LPP, sub = lane % LPP;
-    const int q_mine = t.q0 + ps;
-    const int K = p.K;
-    const int KC = K < kMaxItems / PPW ? K : kMaxItems / PPW;
-    const rsrc_t vr = make_rsrc(p.value, p.value_bytes);
-    T* out = static_cast<T*>(p.out);
-
-    for (int c0 = 0; c0 < p.D; c0 += LPP * VEC) {
-        const int chan = c0 + sub * VEC;
-        const bool active = chan < p.D;
-        const uint32_t chan_bytes = (uint32_t)chan << Row<T, VEC>::kShift;
-        float acc[VEC];
-#pragma unroll
-        for (int i = 0; i < VEC; ++i) acc[i] = 0.f;
-
-        for (int k0 = 0; k0 < K; k0 += KC) {
-            const int kn = K - k0 < KC ? K - k0 : KC;
-            wave_lds_sync();
-            for (int j = lane; j < PPW * kn; j += 64) {
-                const int jq = j / kn, jk = j - jq * kn;
-                SampleDesc sd;
-                describe(p, s_lvl, t.n, t.m, t.q0 + jq, k0 + jk, true, sd);
-                s_off[wave][j] = sd.off;
-                s_w[wave][j] = sd.w;
-            }
-            wave_lds_sync();
-            if (active) {
-                const int base = ps * kn;
-#pragma unroll 4
-                for (int kk = 0; kk < kn; ++kk) {
-                    const int4 off = s_off[wave][base + kk];
-                    const float4 w = s_w[wave][base + kk];
-                    float v0[VEC], v1[VEC], v2[VEC], v3[VEC];
-                    Row<T, VEC>::load(v0, vr, ((uint32_t)off.x << Row<T, VEC>::kShift) + chan_bytes);
-                    Row<T, VEC>::load(v1, vr, ((uint32_t)off.y << Row<T, VEC>::kShift) + chan_bytes);
-                    Row<T, VEC>::load(v2, vr, ((uint32_t)off.z << Row<T, VEC>::kShift) + chan_bytes);
-                    Row<T, VEC>::load(v3, vr, ((uint32_t)off.w << Row<T, VEC>::kShift) + chan_bytes);
-#pragma unroll
-                    for (int i = 0; i < VEC; ++i)
-                        acc[i] += w.x * v0[i] + w.y * v1[i] + w.z * v2[i] + w.w * v3[i];
-                }
-            }
-        }
-        if (active && q_mine < p.Lq)
-            Row<T, VEC>::store(out + ((size_t)(t.n * p.Lq + q_mine) * p.M + t.m) * p.D + chan, acc);
-    }
-}
-
-// ---------------------------------------------------------------- backward
-
-template <typename T, int VEC, int LPP>
-__global__ __launch_bounds__(kBlock) void bwd_kernel(Params p) {
-    constexpr int PPW = 64 / LPP;
-    __shared__ int s_lvl[3 * kMaxLevels];
-    __shared__ int4 s_off[kWaves][kMaxItems];
-    __shared__ float4 s_w[kWaves][kMaxItems];
-    __shared__ float4 s_x[kWaves][kMaxItems];  // {a, lh, lw, -} in, {grad_attn, gx, gy, -} out
-    load_levels(p, s_lvl);
-
-    Tile t;
-    if (!tile_of(p, PPW, t)) return;
-    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-    const int ps = lane / LPP, sub = lane % LPP;
-    const int K = p.K;
-    const int KC = K < kMaxItems / PPW ? K : kMaxItems / PPW;
-    const rsrc_t vr = make_rsrc(p.value, p.value_bytes);
-    const rsrc_t gr = make_rsrc(p.grad_value, p.gv_bytes);
-    const T* gout = static_cast<const T*>(p.grad_out);
-    const int q_mine = t.q0 + ps;
-    const bool q_ok = q_mine < p.Lq;
-    const size_t gout_row = ((size_t)(t.n * p.Lq + (q_ok ? q_mine : 0)) * p.M + t.m) * p.D;
-
-    for (int k0 = 0; k0 < K; k0 += KC) {
-        const int kn = K - k0 < KC ? K - k0 : KC;
-        wave_lds_sync();
-        for (int j = lane; j < PPW * kn; j += 64) {
-            const int jq = j / kn, jk = j - jq * kn;
-            SampleDesc sd;
-            describe(p, s_lvl, t.n, t.m, t.q0 + jq, k0 + jk, false, sd);
-            s_off[wave][j] = sd.off;
-            s_w[wave][j] = sd.w;
-            s_x[wave][j] = make_float4(sd.a, sd.lh, sd.lw, 0.f);
-        }
-        wave_lds_sync();
-        const int base = ps * kn;
-        for (int kk = 0; kk < kn; ++kk) {
-            const int4 off = s_off[wave][base + kk];
-            const float4 w = s_w[wave][base + kk];
-            const float4 x = s_x[wave][base + kk];
-            const float a = x.x, lh = x.y, lw = x.z, hh = 1.f - lh, hw = 1.f - lw;
-            float ga = 0.f, gw = 0.f, gh = 0.f;
-            for (int c0 = 0; c0 < p.D; c0 += LPP * VEC) {
-                const int chan = c0 + sub * VEC;
-                if (chan < p.D) {
-                    const uint32_t cb = (uint32_t)chan << Row<T, VEC>::kShift;
-                    float g[VEC], v0[VEC], v1[VEC], v2[VEC], v3[VEC];
-                    Row<T, VEC>::load_ptr(g, gout + gout_row + chan);
-                    Row<T, VEC>::load(v0, vr, ((uint32_t)off.x << Row<T, VEC>::kShift) + cb);
-                    Row<T, VEC>::load(v1, vr, ((uint32_t)off.y << Row<T, VEC>::kShift) + cb);
-                    Row<T, VEC>::load(v2, vr, ((uint32_t)off.z << Row<T, VEC>::kShift) + cb);
-                    Row<T, VEC>::load(v3, vr, ((uint32_t)off.w << Row<T, VEC>::kShift) + cb);
-#pragma unroll
-                    for (int i = 0; i < VEC; ++i) {
-                        const float s = w.x * v0[i] + w.y * v1[i] + w.z * v2[i] + w.w * v3[i];
-                        ga += g[i] * s;
-                        gw += g[i] * (hh * (v1[i] - v0[i]) + lh * (v3[i] - v2[i]));
-                        gh += g[i] * (hw * (v2[i] - v0[i]) + lw * (v3[i] - v1[i]));
-                    }
-                    // grad_value[corner] += a * w_corner * g   (fp32 rows)
-                    const uint32_t gcb = (uint32_t)chan << 2;
-                    const float a0 = a * w.x, a1 = a * w.y, a2 = a * w.z, a3 = a * w.w;
-#pragma unroll
-                    for (int i = 0; i < VEC; ++i) {
-                        const uint32_t ci = gcb + 4u * i;
-                        __builtin_amdgcn_raw_ptr_buffer_atomic_fadd_f32(a0 * g[i], gr, ((uint32_t)off.x << 2) + ci, 0, 0);
-                        __builtin_amdgcn_raw_ptr_buffer_atomic_fadd_f32(a1 * g[i], gr, ((uint32_t)off.y << 2) + ci, 0, 0);
-                        __builtin_amdgcn_raw_ptr_buffer_atomic_fadd_f32(a2 * g[i], gr, ((uint32_t)off.z << 2) + ci, 0, 0);
-                        __builtin_amdgcn_raw_ptr_buffer_atomic_fadd_f32(a3 * g[i], gr, ((uint32_t)off.w << 2) + ci, 0, 0);
-                    }
-                }
-            }
-            ga = group_sum<LPP>(ga);
-            gw = group_sum<LPP>(gw);
-            gh = group_sum<LPP>(gh);
-            if (sub == 0) {
-                const int l = (k0 + kk) / p.P;
-                const float Wf = (float)s_lvl[kMaxLevels + l], Hf = (float)s_lvl[l];
-                s_x[wave][base + kk] = make_float4(ga, Wf * (a * gw), Hf * (a * gh), 0.f);
-            }
-        }
-        wave_lds_sync();
-        for (int j = lane; j < PPW * kn; j += 64) {
-            const int jq = j / kn, jk = j - jq * kn;
-            const int q = t.q0 + jq;
-            if (q < p.Lq) {
-                const int smp = ((t.n * p.Lq + q) * p.M + t.m) * K + k0 + jk;
-                const float4 r = s_x[wave][j];
-                p.grad_attn[smp] = r.x;
-                reinterpret_cast<float2*>(p.grad_loc)[smp] = make_float2(r.y, r.z);
-            }
-        }
-    }
-}
-
-__global__ __launch_bounds__(256) void zero_kernel(float4* p, int64_t n4, float* tail, int ntail) {
-    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n4; i += stride)
-        p[i] = make_float4(0.f, 0.f, 0.f, 0.f);
-    if (blockIdx.x == 0 && (int)threadIdx.x < ntail) tail[threadIdx.x] = 0.f;
-}
-
-// ---------------------------------------------------------------- dispatch
-
+// Channels per lane: the widest row piece (<= 16 bytes) that divides D.
 template <typename T>
-int pick_vec(int D) {
+inline int pick_vec(int D) {
     constexpr int kMax = 16 / sizeof(T);
     for (int v = kMax; v > 1; v >>= 1)
         if (D % v == 0) return v;
     return 1;
 }
 
-int pick_lpp(int D, int vec) {
+// Lanes per query: enough VEC-wide pieces to cover D, rounded up to a power of two (<= 64).
+inline int pick_lpp(int D, int vec) {
     int need = (D + vec - 1) / vec;
     int lpp = 1;
     while (lpp < need && lpp < 64) lpp <<= 1;
     return lpp;
 }
 
+// Launches KernelT<T, VEC, lpp>::fn() over (slab, query chunk) workgroups of kBlock lanes.
 template <template <typename, int, int> class KernelT, typename T, int VEC>
 hipError_t launch_lpp(Params p, int lpp, hipStream_t stream) {
     auto go = [&](auto kernel, int ppw) -> hipError_t {
@@ -452,15 +275,6 @@ hipError_t launch_lpp(Params p, int lpp, hipStream_t stream) {
     }
 }
 
-template <typename T, int VEC, int LPP>
-struct FwdK {
-    static auto fn() { return fwd_kernel<T, VEC, LPP>; }
-};
-template <typename T, int VEC, int LPP>
-struct BwdK {
-    static auto fn() { return bwd_kernel<T, VEC, LPP>; }
-};
-
 template <template <typename, int, int> class KernelT, typename T>
 hipError_t launch_typed(const Params& p, hipStream_t stream) {
     const int vec = pick_vec<T>(p.D);
@@ -476,25 +290,4 @@ hipError_t launch_typed(const Params& p, hipStream_t stream) {
 }
 
 }  // namespace
-
-hipError_t launch_forward(const Params& p, msda_dtype_t dtype, hipStream_t stream) {
-    return dtype == MSDA_F16 ? launch_typed<FwdK, _Float16>(p, stream) : launch_typed<FwdK, float>(p, stream);
-}
-
-hipError_t launch_backward(const Params& p, msda_dtype_t dtype, hipStream_t stream) {
-    return dtype == MSDA_F16 ? launch_typed<BwdK, _Float16>(p, stream) : launch_typed<BwdK, float>(p, stream);
-}
-
-hipError_t launch_zero(float* ptr, int64_t n, hipStream_t stream) {
-    if (n <= 0) return hipSuccess;
-    const int64_t n4 = n / 4;
-    const int ntail = (int)(n - n4 * 4);
-    int64_t blocks = (n4 + 255) / 256;
-    if (blocks > 8192) blocks = 8192;
-    if (blocks < 1) blocks = 1;
-    hipLaunchKernelGGL(zero_kernel, dim3((unsigned)blocks), dim3(256), 0, stream,
-                       reinterpret_cast<float4*>(ptr), n4, ptr + n4 * 4, ntail);
-    return hipGetLastError();
-}
-
 }  // namespace msda

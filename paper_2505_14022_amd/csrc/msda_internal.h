@@ -1,4 +1,4 @@
-// Internal interface between the C ABI (msda_api.cpp) and the HIP kernels (msda_kernels.hip).
+// Internal interface between the C ABI (msda_api.cpp) and the HIP kernels (msda_*.hip).
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -17,6 +17,14 @@ constexpr int kMaxLevels = MSDA_MAX_LEVELS;
 constexpr int64_t kMaxLaunchElems = int64_t(1) << 29;
 constexpr int64_t kMaxIndex = (int64_t(1) << 31) - 1;
 
+// Owner-computes grad_value: limits of the binned path.
+constexpr int kHistMax = 15872;      // bins of one (n, m) slab counted in LDS (62 KB)
+constexpr int kTileFloats = 3200;    // LDS floats of one tile accumulator with its margin (12.5 KB per wave)
+constexpr int kBinnedMaxD = 355;     // channels per head handled by the binned path (1x1 tiles)
+constexpr int kChunkRecords = 512;   // records folded by one accumulate work item
+constexpr int kCountQueries = 4096;  // samples per workgroup in the counting / scatter passes
+constexpr int kScanTiles = 1024;     // tiles per workgroup in the scan passes
+
 // Everything one launch needs, passed by value as the kernel argument.
 struct Params {
     const void* value;     // [n_batch, S, M, D] dtype (already offset to the first batch item)
@@ -34,10 +42,41 @@ struct Params {
     int chunks;            // ceil(Lq / q_per_block)
     int num_blocks;        // n_batch * M * chunks (the grid is padded to a multiple of 8)
     int H[kMaxLevels], W[kMaxLevels], start[kMaxLevels];
+
+    // ---- binned grad_value (owner-computes); filled by plan_binned() ----
+    int tile_lh[kMaxLevels];    // log2 of the tile height at level l
+    int tile_lw[kMaxLevels];    // log2 of the tile width at level l
+    int tiles_x[kMaxLevels];    // tiles per tile-row at level l
+    int tile_base[kMaxLevels];  // first tile of level l within a slab
+    int tiles_per_slab;
+    int n_slabs;                // n_batch * M
+    int n_tiles;                // n_slabs * tiles_per_slab
+    int n_samples;              // n_batch * Lq * M * K
+    int max_items;              // capacity of `items`
+    int scan_blocks;            // ceil(n_tiles / kScanTiles)
+    int* counts;                // [n_tiles * 4]       samples per (tile, class)
+    int* offsets;               // [n_tiles * 4 + 1]   exclusive prefix of counts
+    int* cursor;                // [n_tiles * 4]       fill position per bin
+    int* tile_chunks;           // [n_tiles + 1]       exclusive prefix of work items per tile
+    int* items;                 // [max_items]         work item -> tile
+    int* block_sums;            // [2 * scan_blocks]
+    int* records;               // [n_samples]         launch-local sample index, sorted by bin
 };
 
 hipError_t launch_forward(const Params& p, msda_dtype_t dtype, hipStream_t stream);
-hipError_t launch_backward(const Params& p, msda_dtype_t dtype, hipStream_t stream);
+// grad_loc / grad_attn; with `atomic_grad_value` the same kernel also scatters grad_value with
+// fp32 atomics (grad_value must be zero beforehand).
+hipError_t launch_backward_grads(const Params& p, msda_dtype_t dtype, bool atomic_grad_value, hipStream_t stream);
+// grad_value by binning samples per destination tile and accumulating each tile once.
+hipError_t launch_backward_value_binned(const Params& p, msda_dtype_t dtype, hipStream_t stream);
 hipError_t launch_zero(float* ptr, int64_t n, hipStream_t stream);
+
+// Chooses tile sizes for the binned grad_value path and fills the geometry fields of `p`.
+// Returns false if the path does not apply (then grad_value uses atomics).
+bool plan_binned(Params& p);
+// Workspace bytes of the binned path for the geometry in `p` (after plan_binned).
+size_t binned_workspace_bytes(const Params& p);
+// Points the workspace fields of `p` into `ws`.
+void bind_workspace(Params& p, void* ws);
 
 }  // namespace msda

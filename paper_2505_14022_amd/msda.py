@@ -23,8 +23,8 @@ MSDA_F32 = 0
 MSDA_F16 = 1
 MSDA_MAX_LEVELS = 16
 
-EXPORTED = ["msda_check_args", "msda_forward", "msda_backward", "msda_status_string",
-            "msda_last_error", "msda_version"]
+EXPORTED = ["msda_check_args", "msda_forward", "msda_backward", "msda_backward_workspace_size",
+            "msda_status_string", "msda_last_error", "msda_version"]
 
 
 class MsdaError(RuntimeError):
@@ -48,8 +48,11 @@ def lib():
         L.msda_check_args.restype = ctypes.c_int
         L.msda_forward.argtypes = [vp, ip, ip, vp, vp, vp] + [i64] * 7 + [ctypes.c_int, vp]
         L.msda_forward.restype = ctypes.c_int
-        L.msda_backward.argtypes = [vp, ip, ip, vp, vp, vp, vp, vp, vp] + [i64] * 7 + [ctypes.c_int, vp]
+        L.msda_backward.argtypes = [vp, ip, ip, vp, vp, vp, vp, vp, vp, vp, ctypes.c_size_t] + [i64] * 7 + \
+            [ctypes.c_int, vp]
         L.msda_backward.restype = ctypes.c_int
+        L.msda_backward_workspace_size.argtypes = [ip, ip] + [i64] * 7 + [ctypes.c_int, ctypes.POINTER(ctypes.c_size_t)]
+        L.msda_backward_workspace_size.restype = ctypes.c_int
         L.msda_status_string.argtypes = [ctypes.c_int]
         L.msda_status_string.restype = ctypes.c_char_p
         L.msda_last_error.argtypes = []
@@ -129,6 +132,15 @@ def _dims(value, sampling_loc):
     return N, S, M, D, Lq, L, P
 
 
+def workspace_size(spatial_shapes, level_start_index, N, S, M, D, Lq, L, P, dtype) -> int:
+    """msda_backward_workspace_size: bytes of device workspace for the owner-computes grad_value."""
+    sh, st = _host_tables(spatial_shapes, level_start_index)
+    out = ctypes.c_size_t(0)
+    r = lib().msda_backward_workspace_size(_iptr(sh), _iptr(st), N, S, M, D, Lq, L, P, int(dtype), ctypes.byref(out))
+    _raise(r, "msda_backward_workspace_size")
+    return int(out.value)
+
+
 def forward(value, spatial_shapes, level_start_index, sampling_loc, attn_weight, out=None, stream=None):
     """out[N, Lq, M*D] = MSDA(value, sampling_loc, attn_weight), computed by msda_forward."""
     import torch
@@ -144,8 +156,12 @@ def forward(value, spatial_shapes, level_start_index, sampling_loc, attn_weight,
 
 
 def backward(value, spatial_shapes, level_start_index, sampling_loc, attn_weight, grad_out,
-             grad_value=None, grad_loc=None, grad_attn=None, stream=None):
-    """(grad_value fp32, grad_loc, grad_attn) from msda_backward."""
+             grad_value=None, grad_loc=None, grad_attn=None, workspace="auto", stream=None):
+    """(grad_value fp32, grad_loc, grad_attn) from msda_backward.
+
+    workspace: "auto" allocates the size msda_backward_workspace_size reports (a uint8 device
+    tensor), None passes no workspace (grad_value by atomics), or a caller-owned uint8 tensor.
+    """
     import torch
 
     N, S, M, D, Lq, L, P = _dims(value, sampling_loc)
@@ -157,8 +173,13 @@ def backward(value, spatial_shapes, level_start_index, sampling_loc, attn_weight
     if grad_attn is None:
         grad_attn = torch.empty(tuple(attn_weight.shape), dtype=torch.float32, device=dev)
     sh, st = _host_tables(spatial_shapes, level_start_index)
+    if isinstance(workspace, str) and workspace == "auto":
+        nbytes = workspace_size(sh.reshape(-1, 2), st, N, S, M, D, Lq, L, P, _dtype_code(value))
+        workspace = torch.empty(max(nbytes, 1), dtype=torch.uint8, device=dev) if nbytes else None
+    ws_ptr = _dptr(workspace) if workspace is not None else None
+    ws_bytes = workspace.numel() * workspace.element_size() if workspace is not None else 0
     r = lib().msda_backward(_dptr(value), _iptr(sh), _iptr(st), _dptr(sampling_loc), _dptr(attn_weight),
-                            _dptr(grad_out), _dptr(grad_value), _dptr(grad_loc), _dptr(grad_attn),
+                            _dptr(grad_out), _dptr(grad_value), _dptr(grad_loc), _dptr(grad_attn), ws_ptr, ws_bytes,
                             N, S, M, D, Lq, L, P, _dtype_code(value), _stream(stream))
     _raise(r, "msda_backward")
     return grad_value, grad_loc, grad_attn
@@ -172,8 +193,8 @@ def forward_raw(value_ptr: int, shapes: np.ndarray, starts: np.ndarray, loc_ptr:
 
 
 def backward_raw(value_ptr: int, shapes: np.ndarray, starts: np.ndarray, loc_ptr: int, attn_ptr: int,
-                 gout_ptr: int, gv_ptr: int, gl_ptr: int, ga_ptr: int, dims: Sequence[int], dtype: int,
-                 stream: int) -> int:
+                 gout_ptr: int, gv_ptr: int, gl_ptr: int, ga_ptr: int, ws_ptr: Optional[int], ws_bytes: int,
+                 dims: Sequence[int], dtype: int, stream: int) -> int:
     """msda_backward on raw device addresses; returns the status (used by the benchmark loop)."""
     return lib().msda_backward(value_ptr, _iptr(shapes), _iptr(starts), loc_ptr, attn_ptr, gout_ptr,
-                               gv_ptr, gl_ptr, ga_ptr, *dims, dtype, stream)
+                               gv_ptr, gl_ptr, ga_ptr, ws_ptr, ws_bytes, *dims, dtype, stream)

@@ -59,14 +59,16 @@ def to_device(inp: workloads.Inputs) -> DeviceInputs:
                         attn=torch.from_numpy(inp.attn).to(dev), grad_out=torch.from_numpy(inp.grad_out).to(dev))
 
 
-def run_gpu(inp: workloads.Inputs, backward: bool = True):
+def run_gpu(inp: workloads.Inputs, backward: bool = True, workspace="auto"):
+    """Run libmsda on `inp`; workspace="auto" takes the owner-computes grad_value path, None the
+    atomic one."""
     import torch
 
     d = to_device(inp)
     out = msda.forward(d.value, inp.shapes, inp.starts, d.loc, d.attn)
     res = {"out": out}
     if backward:
-        gv, gl, ga = msda.backward(d.value, inp.shapes, inp.starts, d.loc, d.attn, d.grad_out)
+        gv, gl, ga = msda.backward(d.value, inp.shapes, inp.starts, d.loc, d.attn, d.grad_out, workspace=workspace)
         res.update(grad_value=gv, grad_loc=gl, grad_attn=ga)
     torch.cuda.synchronize()
     return {k: v.float().cpu().numpy() if k != "out" else v.cpu().numpy() for k, v in res.items()}
@@ -81,10 +83,10 @@ def run_oracle(inp: workloads.Inputs, backward: bool = True):
     return res
 
 
-def check_parity(inp: workloads.Inputs, backward: bool = True, gpu=None, ref=None):
+def check_parity(inp: workloads.Inputs, backward: bool = True, gpu=None, ref=None, workspace="auto"):
     """Element-by-element comparison of every output; returns the error table."""
     fp16 = inp.value.dtype == np.float16
-    gpu = gpu or run_gpu(inp, backward)
+    gpu = gpu or run_gpu(inp, backward, workspace)
     ref = ref or run_oracle(inp, backward)
     errs = {"out": normwise(gpu["out"], ref["out"])}
     tols = {"out": TOL_OUT_F16 if fp16 else TOL_OUT_F32}

@@ -146,8 +146,33 @@ def test_backward_checks_pointers_before_launching(L):
     a = base()
     ip = ctypes.POINTER(ctypes.c_int64)
     r = L.msda_backward(None, a[0].ctypes.data_as(ip), a[1].ctypes.data_as(ip), None, None, None, None, None,
-                        None, *a[2:9], a[9], None)
+                        None, None, 0, *a[2:9], a[9], None)
     assert r == msda.MSDA_ERROR_INVALID_VALUE
     r = L.msda_backward(0x1000, a[0].ctypes.data_as(ip), a[1].ctypes.data_as(ip), 0x2000, 0x3000, 0x4000,
-                        0x5008, 0x6000, 0x7000, *a[2:9], a[9], None)
+                        0x5008, 0x6000, 0x7000, None, 0, *a[2:9], a[9], None)
     assert r == msda.MSDA_ERROR_INVALID_VALUE and "grad_value" in msda.last_error()
+    # a workspace smaller than reported is rejected before anything is launched
+    need = msda.workspace_size(a[0], a[1], *a[2:9], a[9])
+    assert need > 0
+    r = L.msda_backward(0x1000, a[0].ctypes.data_as(ip), a[1].ctypes.data_as(ip), 0x2000, 0x3000, 0x4000,
+                        0x5000, 0x6000, 0x7000, 0x8000, need - 1, *a[2:9], a[9], None)
+    assert r == msda.MSDA_ERROR_INVALID_VALUE and "workspace" in msda.last_error()
+    r = L.msda_backward(0x1000, a[0].ctypes.data_as(ip), a[1].ctypes.data_as(ip), 0x2000, 0x3000, 0x4000,
+                        0x5000, 0x6000, 0x7000, 0x8010, need, *a[2:9], a[9], None)
+    assert r == msda.MSDA_ERROR_INVALID_VALUE and "aligned" in msda.last_error()
+
+
+@pytest.mark.parametrize("w", workloads.WORKLOADS, ids=lambda w: w.name)
+def test_workspace_sizes(L, w):
+    need = msda.workspace_size(*_args(w))
+    # the owner-computes path applies to every workload; its scratch is a few bytes per sample
+    assert 0 < need < 64 + 8 * w.samples + 64 * w.N * w.M * w.S, need
+
+
+def test_workspace_size_not_applicable(L):
+    a = base()
+    a[5] = 3000  # D > 2048: grad_value by atomics, no workspace
+    assert msda.workspace_size(a[0], a[1], *a[2:9], a[9]) == 0
+    a = base()
+    a[6] = 0  # nothing to do
+    assert msda.workspace_size(a[0], a[1], *a[2:9], a[9]) == 0

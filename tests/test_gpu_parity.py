@@ -42,11 +42,22 @@ SMALL = [
 ]
 
 
+@pytest.mark.parametrize("path", ["binned", "atomic"])
 @pytest.mark.parametrize("case", SMALL, ids=lambda c: f"N{c[0]}M{c[1]}D{c[2]}L{len(c[3])}P{c[4]}Lq{c[5]}{c[6]}")
-def test_small_parity(case):
+def test_small_parity(case, path):
     N, M, D, shapes, P, Lq, dt = case
     inp = workloads.random_case(N, M, D, shapes, P, Lq, dt, seed=1000 + D + Lq)
-    say(f"small case {inp.w.name}")
+    say(f"small case {inp.w.name} ({path} grad_value)")
+    check_parity(inp, workspace="auto" if path == "binned" else None)
+
+
+@pytest.mark.parametrize("seed", range(3))
+def test_dense_coarse_levels_split_tiles(seed):
+    # many queries on small maps: tiles see more samples than one work item folds, so tiles are
+    # split and their rows are added with atomics
+    inp = workloads.random_case(2, 4, 32, ((12, 10), (3, 5), (1, 2)), 8, 3000, "f32", seed=40 + seed,
+                                lo=0.2, hi=0.6)
+    say(f"split tiles seed {seed}")
     check_parity(inp)
 
 
@@ -57,11 +68,17 @@ def test_location_ranges(lo, hi):
     check_parity(inp)
 
 
-@pytest.mark.parametrize("w", workloads.WORKLOADS[:5], ids=lambda w: w.name)
+@pytest.mark.parametrize("w", workloads.WORKLOADS, ids=lambda w: w.name)
 def test_workload_full_size(w):
     say(f"full-size workload {w.name}: N={w.N} M={w.M} D={w.D} S={w.S} Lq={w.Lq} L={w.L} P={w.P} {w.dtype}")
     inp = workloads.generate(w)
     check_parity(inp)
+
+
+def test_workload_full_size_atomic_path():
+    w = workloads.BY_NAME["detr_encoder"]
+    say(f"full-size workload {w.name} with atomic grad_value")
+    check_parity(workloads.generate(w), workspace=None)
 
 
 def test_pixel_centres_are_exact():
