@@ -335,9 +335,12 @@ template <typename T, int DC>
 __global__ __launch_bounds__(256) void fold_kernel(Params p, int tile_floats) {
     extern __shared__ float s_acc_all[];
     __shared__ int s_geo[kGeo * kMaxLevels];
+    __shared__ float4 s_w[kAccWaves][kFoldBatch];  // a * bilinear weights of the batch's records
     load_geo(p, s_geo);
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
     float* acc = s_acc_all + wave * tile_floats;
+    // lanes 0-31 read (w00, w01) of a record, lanes 32-63 (w10, w11)
+    const float2* s_wrow = reinterpret_cast<const float2*>(&s_w[wave][0]) + (lane >> 5);
     const int total = p.tile_chunks[p.n_tiles];
     const int nwaves = gridDim.x * kAccWaves;
     const T* gout = static_cast<const T*>(p.grad_out);
@@ -415,6 +418,9 @@ __global__ __launch_bounds__(256) void fold_kernel(Params p, int tile_floats) {
                 w10 = a * (lh * hw);
                 w11 = a * (lh * lw);
             }
+            wave_lds_sync();  // the previous batch is done with s_w
+            s_w[wave][lane] = make_float4(w00, w01, w10, w11);
+            wave_lds_sync();
             // bit r: the 2x2 footprints of records r and r+1 do not overlap, so both can be
             // read before either is written back
             const int nrow = __shfl_down(prow, 1, 64), ncol = __shfl_down(pcol, 1, 64);
@@ -435,14 +441,12 @@ __global__ __launch_bounds__(256) void fold_kernel(Params p, int tile_floats) {
                 for (int r = 0; r < kFoldBatch; r += 2) {
                     if (r >= cnt) continue;
                     float* da = lane_acc + lane_i(pk, r) * D;
-                    const float a00 = lane_f(w00, r), a01 = lane_f(w01, r);
-                    const float a10 = lane_f(w10, r), a11 = lane_f(w11, r);
-                    const float wla = half ? a10 : a00, wra = half ? a11 : a01;
+                    const float2 wa = s_wrow[2 * r];
+                    const float wla = wa.x, wra = wa.y;
                     if (r + 1 < cnt) {
                         float* db = lane_acc + lane_i(pk, r + 1) * D;
-                        const float b00 = lane_f(w00, r + 1), b01 = lane_f(w01, r + 1);
-                        const float b10 = lane_f(w10, r + 1), b11 = lane_f(w11, r + 1);
-                        const float wlb = half ? b10 : b00, wrb = half ? b11 : b01;
+                        const float2 wb = s_wrow[2 * (r + 1)];
+                        const float wlb = wb.x, wrb = wb.y;
                         if ((apart >> r) & 1) {
                             const float a0v = da[0], a1v = da[D], b0v = db[0], b1v = db[D];
                             da[0] = a0v + wla * gr[r];
@@ -480,19 +484,243 @@ __global__ __launch_bounds__(256) void fold_kernel(Params p, int tile_floats) {
     }
 }
 
+// ---------------------------------------------------------------- 4. fold by gathering (D % 4 == 0)
+
+constexpr int kTilePix = 64;                    // pixels of an 8x8 tile
+constexpr int kMaxContrib = 4 * kChunkRecords;  // a record adds to at most four pixels of a tile
+
+template <typename T, int VEC>
+struct QuadBuf;
+template <>
+struct QuadBuf<float, 4> {
+    static __device__ __forceinline__ float4 load(rsrc_t r, uint32_t off_elems) {
+        auto x = __builtin_amdgcn_raw_buffer_load_b128(r, off_elems << 2, 0, 0);
+        const uint32_t u0 = x[0], u1 = x[1], u2 = x[2], u3 = x[3];
+        return make_float4(as_float(u0), as_float(u1), as_float(u2), as_float(u3));
+    }
+};
+template <>
+struct QuadBuf<_Float16, 4> {
+    static __device__ __forceinline__ float4 load(rsrc_t r, uint32_t off_elems) {
+        auto x = __builtin_amdgcn_raw_buffer_load_b64(r, off_elems << 1, 0, 0);
+        const uint32_t u0 = x[0], u1 = x[1];
+        float4 f;
+        unpack_h2(u0, f.x, f.y);
+        unpack_h2(u1, f.z, f.w);
+        return f;
+    }
+};
+
+// One wave per work item (a tile, or a chunk of a split tile's visible records):
+//   1. every lane describes kChunkRecords/64 records (all their loads in flight together) and
+//      expands each into its contributions to the tile's pixels (corners that fall on the tile
+//      and on the map), counting them per pixel in LDS;
+//   2. a 64-entry scan (one pixel per lane) turns the counts into per-pixel list starts;
+//   3. every contribution (grad_out row, a * corner weight) is placed in its pixel's list;
+//   4. eight lanes serve one pixel (four channels each) and sum its list in registers, sixteen
+//      row reads in flight per lane; reads past a list's end use an out-of-range buffer offset,
+//      which returns zeros, so no lane branches.
+// Each on-map pixel of the tile is stored once (plain store), or added with atomics for split tiles.
+template <typename T>
+__global__ __launch_bounds__(256) void fold_gather_kernel(Params p) {
+    __shared__ int s_geo[kGeo * kMaxLevels];
+    __shared__ int s_start[kAccWaves][kTilePix + 1];
+    __shared__ int2 s_c[kAccWaves][kMaxContrib];  // (grad_out row, bit pattern of the weight)
+    load_geo(p, s_geo);
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    int* start = s_start[wave];
+    int2* sc = s_c[wave];
+    const int total = p.tile_chunks[p.n_tiles];
+    const int nwaves = gridDim.x * kAccWaves;
+    const int D = p.D;
+    const rsrc_t gr = make_rsrc(p.grad_out, (uint32_t)((size_t)p.n_batch * p.Lq * p.M * D * sizeof(T)));
+    const int quad = lane & 7, pgrp = lane >> 3;
+
+    for (int item = blockIdx.x * kAccWaves + wave; item < total; item += nwaves) {
+        const int t = __builtin_amdgcn_readfirstlane(p.items[item]);
+        if (t < 0 || t >= p.n_tiles) continue;  // never taken: items holds tile indices
+        const int first = __builtin_amdgcn_readfirstlane(p.tile_chunks[t]);
+        const int nitems = __builtin_amdgcn_readfirstlane(p.tile_chunks[t + 1]) - first;
+        const int chunk = item - first;
+        const int slab = t / p.tiles_per_slab, tin = t - slab * p.tiles_per_slab;
+        const int n = slab / p.M, m = slab - n * p.M;
+        const int l = __builtin_amdgcn_readfirstlane(level_of_tile(s_geo, p.L, tin));
+        const int H = __builtin_amdgcn_readfirstlane(s_geo[l]);
+        const int W = __builtin_amdgcn_readfirstlane(s_geo[kMaxLevels + l]);
+        const int th = __builtin_amdgcn_readfirstlane(s_geo[2 * kMaxLevels + l]);
+        const int tw = __builtin_amdgcn_readfirstlane(s_geo[3 * kMaxLevels + l]);
+        const int TH = 1 << th, TW = 1 << tw;
+        const int rel = tin - __builtin_amdgcn_readfirstlane(s_geo[5 * kMaxLevels + l]);
+        const int txn = __builtin_amdgcn_readfirstlane(s_geo[4 * kMaxLevels + l]);
+        const int ty = rel / txn, tx = rel - ty * txn;
+        const int h_org = ty << th, w_org = tx << tw;
+        const int st = __builtin_amdgcn_readfirstlane(s_geo[6 * kMaxLevels + l]);
+        const float Hf = (float)H, Wf = (float)W;
+        // pixels of the tile that exist on the map
+        const int th_on = min(TH, H - h_org), tw_on = min(TW, W - w_org);
+
+        const TileInfo ti = tile_info(p, s_geo, t);
+        const int a0 = p.offsets[ti.own0], a1 = p.offsets[ti.own1];
+        const int b0 = ti.l1 > ti.l0 ? p.offsets[ti.l0] : 0, b1 = ti.l1 > ti.l0 ? p.offsets[ti.l1] : 0;
+        const int c0 = ti.u1 > ti.u0 ? p.offsets[ti.u0] : 0, c1 = ti.u1 > ti.u0 ? p.offsets[ti.u1] : 0;
+        const int d0 = ti.d1 > ti.d0 ? p.offsets[ti.d0] : 0, d1 = ti.d1 > ti.d0 ? p.offsets[ti.d1] : 0;
+        const int na = __builtin_amdgcn_readfirstlane(a1 - a0), nb = __builtin_amdgcn_readfirstlane(b1 - b0);
+        const int nc = __builtin_amdgcn_readfirstlane(c1 - c0), nd = __builtin_amdgcn_readfirstlane(d1 - d0);
+        const int nvis = na + nb + nc + nd;
+        const int beg = __builtin_amdgcn_readfirstlane(chunk * kChunkRecords);
+        const int end = __builtin_amdgcn_readfirstlane(min(beg + kChunkRecords, nvis));
+
+        // 1. describe the records and count their contributions per pixel
+        constexpr int kRecPerLane = kChunkRecords / 64;
+        int rrow[kRecPerLane], rpx[kRecPerLane];  // grad_out row; pixel of corner 00 (tile coords, packed)
+        float4 rw[kRecPerLane];
+        {
+            int smp[kRecPerLane];
+#pragma unroll
+            for (int i = 0; i < kRecPerLane; ++i) {
+                int pos = beg + i * 64 + lane, idx = -1;
+                if (pos < end) {
+                    if (pos < na) idx = a0 + pos;
+                    else if ((pos -= na) < nb) idx = b0 + pos;
+                    else if ((pos -= nb) < nc) idx = c0 + pos;
+                    else idx = d0 + (pos - nc);
+                }
+                smp[i] = idx >= 0 && idx < p.n_samples ? p.records[idx] : -1;
+            }
+#pragma unroll
+            for (int i = 0; i < kRecPerLane; ++i) {
+                rpx[i] = -1;
+                if (smp[i] >= 0 && smp[i] < p.n_samples) {
+                    const float2 xy = reinterpret_cast<const float2*>(p.loc)[smp[i]];
+                    const float a = p.attn[smp[i]];
+                    const float w_im = __builtin_fmaf(xy.x, Wf, -0.5f);
+                    const float h_im = __builtin_fmaf(xy.y, Hf, -0.5f);
+                    const float h0f = floorf(h_im), w0f = floorf(w_im);
+                    const float lh = h_im - h0f, lw = w_im - w0f;
+                    const float hh = 1.f - lh, hw = 1.f - lw;
+                    // tile coordinates of corner 00, offset by one so they are >= 0
+                    rpx[i] = (((int)h0f - h_org + 1) << 8) | ((int)w0f - w_org + 1);
+                    rrow[i] = (smp[i] / p.K) * D;
+                    rw[i] = make_float4(a * (hh * hw), a * (hh * lw), a * (lh * hw), a * (lh * lw));
+                }
+            }
+        }
+        wave_lds_sync();
+        start[lane] = 0;
+        if (lane == 0) start[kTilePix] = 0;
+        wave_lds_sync();
+        int rank[kRecPerLane][4];
+#pragma unroll
+        for (int i = 0; i < kRecPerLane; ++i) {
+#pragma unroll
+            for (int c = 0; c < 4; ++c) {
+                rank[i][c] = -1;
+                if (rpx[i] >= 0) {
+                    const int pr = (rpx[i] >> 8) - 1 + (c >> 1), pc = (rpx[i] & 0xff) - 1 + (c & 1);
+                    if (pr >= 0 && pr < th_on && pc >= 0 && pc < tw_on) rank[i][c] = atomicAdd(&start[pr * TW + pc], 1);
+                }
+            }
+        }
+        wave_lds_sync();
+        // 2. per-pixel list starts (one pixel per lane)
+        const int cntp = lane < TH * TW ? start[lane] : 0;
+        int incl = cntp;
+        for (int o = 1; o < 64; o <<= 1) {
+            const int u = __shfl_up(incl, o, 64);
+            if (lane >= o) incl += u;
+        }
+        wave_lds_sync();
+        start[lane] = incl - cntp;
+        if (lane == 63) start[kTilePix] = incl;
+        wave_lds_sync();
+        // 3. place the contributions
+#pragma unroll
+        for (int i = 0; i < kRecPerLane; ++i) {
+#pragma unroll
+            for (int c = 0; c < 4; ++c) {
+                if (rank[i][c] >= 0) {
+                    const int pr = (rpx[i] >> 8) - 1 + (c >> 1), pc = (rpx[i] & 0xff) - 1 + (c & 1);
+                    const float wc = c == 0 ? rw[i].x : c == 1 ? rw[i].y : c == 2 ? rw[i].z : rw[i].w;
+                    const int at = start[pr * TW + pc] + rank[i][c];
+                    if (at < kMaxContrib) sc[at] = make_int2(rrow[i], __builtin_bit_cast(int, wc));
+                }
+            }
+        }
+        wave_lds_sync();
+        // 4. gather: eight lanes per pixel, eight pixels per pass
+        const bool split = nitems > 1;
+        for (int px0 = 0; px0 < TH * TW; px0 += 8) {
+            const int px = px0 + pgrp;
+            const bool px_ok = px < TH * TW;
+            const int r = px >> tw, c = px & (TW - 1);
+            const int s0 = px_ok ? start[px] : 0;
+            const int nq = px_ok ? start[px + 1] - s0 : 0;
+            int nmax = nq;
+            for (int o = 32; o > 0; o >>= 1) nmax = max(nmax, __shfl_xor(nmax, o, 64));
+            const int h = h_org + r, w = w_org + c;
+            for (int ch0 = 0; ch0 < D; ch0 += 32) {
+                const int ch = ch0 + 4 * quad;
+                const bool ch_ok = ch < D;
+                float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+                constexpr int kU = 16;
+                for (int j0 = 0; j0 < nmax; j0 += kU) {
+                    float wt[kU];
+                    uint32_t off[kU];
+#pragma unroll
+                    for (int u = 0; u < kU; ++u) {
+                        const int j = j0 + u;
+                        const bool act = j < nq && ch_ok;
+                        const int2 e = sc[act ? s0 + j : 0];
+                        wt[u] = act ? __builtin_bit_cast(float, e.y) : 0.f;
+                        off[u] = act ? (uint32_t)(e.x + ch) : (uint32_t)kOOBElem;  // zeros past the list
+                    }
+                    float4 g[kU];
+#pragma unroll
+                    for (int u = 0; u < kU; ++u) g[u] = QuadBuf<T, 4>::load(gr, off[u]);
+#pragma unroll
+                    for (int u = 0; u < kU; ++u) {
+                        acc.x += wt[u] * g[u].x;
+                        acc.y += wt[u] * g[u].y;
+                        acc.z += wt[u] * g[u].z;
+                        acc.w += wt[u] * g[u].w;
+                    }
+                }
+                if (px_ok && ch_ok && r < th_on && c < tw_on) {
+                    float* dst = p.grad_value + ((size_t)(n * p.S + st + h * W + w) * p.M + m) * D + ch;
+                    if (split) {
+                        unsafeAtomicAdd(dst + 0, acc.x);
+                        unsafeAtomicAdd(dst + 1, acc.y);
+                        unsafeAtomicAdd(dst + 2, acc.z);
+                        unsafeAtomicAdd(dst + 3, acc.w);
+                    } else {
+                        *reinterpret_cast<float4*>(dst) = acc;
+                    }
+                }
+            }
+        }
+    }
+}
+
 }  // namespace
 
 // ---------------------------------------------------------------- host side
 
 bool plan_binned(Params& p) {
     if (p.D > kBinnedMaxD || p.Lq == 0 || p.K > kCountQueries) return false;
+    // grad_out is read through a buffer resource whose out-of-range offset is kOOBElem
+    if ((int64_t)p.n_batch * p.Lq * p.M * p.D >= kMaxLaunchElems) return false;
     // largest square tile (2^e x 2^e pixels) whose accumulator, with its one-pixel margin, fits
     auto padded = [&](int eh, int ew) { return ((1 << eh) + 2) * ((1 << ew) + 2) * p.D; };
-    if (padded(0, 0) > kTileFloats) return false;
+    if (p.D % 4 != 0 && padded(0, 0) > kTileFloats) return false;
     int e_max = 0;
     while (e_max < 3 && padded(e_max + 1, e_max + 1) <= kTileFloats) ++e_max;
     int lh[kMaxLevels], lw[kMaxLevels];
+    const bool gather = p.D % 4 == 0;  // fold_gather_kernel: 8x8 tiles everywhere
     for (int l = 0; l < p.L; ++l) {
+        if (gather) {
+            lh[l] = lw[l] = 3;
+            continue;
+        }
         // corner hits per pixel of one (n, m) slab if locations were spread evenly; a sample is
         // recorded once (in the tile of its top-left corner), so records per pixel ~ hits / 4
         // plus the ~25% that straddle into neighbours
@@ -608,6 +836,13 @@ hipError_t launch_backward_value_binned(const Params& p0, msda_dtype_t dtype, hi
     }
     const size_t lds = (size_t)kAccWaves * tile_floats * sizeof(float);
     const int fold_blocks = 768;  // three workgroups per CU are resident (LDS-bound)
+    if (p.D % 4 == 0) {
+        if (dtype == MSDA_F16)
+            hipLaunchKernelGGL(fold_gather_kernel<_Float16>, dim3(fold_blocks), dim3(256), 0, stream, p);
+        else
+            hipLaunchKernelGGL(fold_gather_kernel<float>, dim3(fold_blocks), dim3(256), 0, stream, p);
+        return hipGetLastError();
+    }
     const bool d32 = p.D == 32;
     if (dtype == MSDA_F16) {
         if (d32) hipLaunchKernelGGL((fold_kernel<_Float16, 32>), dim3(fold_blocks), dim3(256), lds, stream, p, tile_floats);

@@ -106,5 +106,12 @@ def check_parity(inp: workloads.Inputs, backward: bool = True, gpu=None, ref=Non
     for k in errs:
         assert gpu[k].shape == tuple(ref[k].shape), f"{k}: shape {gpu[k].shape} vs {ref[k].shape}"
         assert np.all(np.isfinite(gpu[k])), f"{inp.w.name}: non-finite values in {k}"
-        assert errs[k] <= tols[k], f"{inp.w.name}: {k} normwise error {errs[k]:.3e} > {tols[k]:.0e}"
+        if errs[k] > tols[k]:
+            d = np.abs(gpu[k].astype(np.float64) - ref[k])
+            i = np.unravel_index(int(np.argmax(d)), d.shape)
+            nbad = int(np.sum(d > tols[k] * max(float(np.max(np.abs(ref[k]))), 1e-30)))
+            ratio = float(np.sum(gpu[k] * ref[k]) / max(float(np.sum(ref[k] * ref[k])), 1e-30))
+            raise AssertionError(f"{inp.w.name}: {k} normwise error {errs[k]:.3e} > {tols[k]:.0e}; worst at {i}: "
+                                 f"gpu {float(gpu[k][i]):.6g} ref {float(ref[k][i]):.6g}; {nbad} of {d.size} "
+                                 f"elements off; <gpu,ref>/<ref,ref> = {ratio:.4f}")
     return errs
