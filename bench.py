@@ -94,6 +94,9 @@ def main():
     ap.add_argument("--workload", default="detr_encoder", choices=sorted(workloads.BY_NAME))
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-compulsory", action="store_true", help="skip counting touched rows (faster)")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                    help="instead of the benchmark, copy a MIB-mebibyte fp32 buffer 5 times (a plain copy kernel of "
+                         "known size, used to scale FETCH_SIZE / WRITE_SIZE counters)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported (MSDA shards over batch "
@@ -105,6 +108,15 @@ def main():
     if not torch.cuda.is_available():
         print("no GPU visible", file=sys.stderr)
         sys.exit(1)
+    if args.copy_calibration:
+        n = args.copy_calibration << 18  # fp32 elements
+        src = torch.ones(n, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(5):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_calibration_bytes_per_direction": n * 4, "copies": 5}))
+        return
     msda.lib()
 
     w = workloads.BY_NAME[args.workload]

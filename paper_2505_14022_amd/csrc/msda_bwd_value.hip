@@ -17,6 +17,8 @@
 //               sample (own bin plus the left / up / up-left neighbours' straddling classes)
 //               and stores the tile's grad_value rows; items of a split tile add theirs with
 //               atomics into rows that were zeroed before.
+#include <atomic>
+
 #include "msda_device.hpp"
 
 namespace msda {
@@ -42,11 +44,14 @@ __device__ __forceinline__ void load_geo(const Params& p, int* s) {
 
 // Bin of a sample within its slab (tile * 4 + class), or -1 if the sample is off the map.
 // Uses the same fp32 coordinates as every other kernel, so the bin agrees with the corners.
-__device__ __forceinline__ int sample_bin(const int* g, int l, float2 xy) {
+__device__ __forceinline__ int sample_bin(const int* g, int l, float2 xy, float* h_out = nullptr,
+                                          float* w_out = nullptr) {
     const int H = g[l], W = g[kMaxLevels + l];
     const float Hf = (float)H, Wf = (float)W;
     const float w_im = __builtin_fmaf(xy.x, Wf, -0.5f);
     const float h_im = __builtin_fmaf(xy.y, Hf, -0.5f);
+    if (h_out) *h_out = h_im;
+    if (w_out) *w_out = w_im;
     if (!(h_im > -1.f && w_im > -1.f && h_im < Hf && w_im < Wf)) return -1;
     const int h0 = (int)floorf(h_im), w0 = (int)floorf(w_im);
     const int th = g[2 * kMaxLevels + l], tw = g[3 * kMaxLevels + l];
@@ -283,20 +288,26 @@ __global__ __launch_bounds__(256) void bin_scatter_kernel(Params p) {
     const int nq = min(p.q_per_block, p.Lq - q0);
     const int nsamp = nq * p.K;
     const float2* loc = reinterpret_cast<const float2*>(p.loc);
-    int bins[kScatterRounds], ranks[kScatterRounds], smps[kScatterRounds];
+    int bins[kScatterRounds], ranks[kScatterRounds];
+    int4 rec[kScatterRounds];  // {grad_out row, a, h_im, w_im}: everything the fold needs
 #pragma unroll
     for (int r = 0; r < kScatterRounds; ++r) {
         const int j = threadIdx.x + 256 * r;
         bins[r] = -1;
         ranks[r] = 0;
-        smps[r] = 0;
+        rec[r] = make_int4(0, 0, 0, 0);
         if (j < nsamp) {
             const int jq = j / p.K, k = j - jq * p.K;
-            const int smp = ((n * p.Lq + q0 + jq) * p.M + m) * p.K + k;
-            const int b = sample_bin(s_geo, k / p.P, loc[smp]);
-            smps[r] = smp;
+            const int pair = (n * p.Lq + q0 + jq) * p.M + m;
+            const int smp = pair * p.K + k;
+            float h_im, w_im;
+            const int b = sample_bin(s_geo, k / p.P, loc[smp], &h_im, &w_im);
             bins[r] = b;
-            if (b >= 0) ranks[r] = atomicAdd(&hist[b], 1);
+            if (b >= 0) {
+                ranks[r] = atomicAdd(&hist[b], 1);
+                rec[r] = make_int4(pair * p.D, __builtin_bit_cast(int, p.attn[smp]), __builtin_bit_cast(int, h_im),
+                                   __builtin_bit_cast(int, w_im));
+            }
         }
     }
     __syncthreads();
@@ -306,20 +317,18 @@ __global__ __launch_bounds__(256) void bin_scatter_kernel(Params p) {
         if (c) hist[i] = atomicAdd(&cursor[i], c);
     }
     __syncthreads();
+    int4* records = reinterpret_cast<int4*>(p.records);
 #pragma unroll
     for (int r = 0; r < kScatterRounds; ++r) {
         if (bins[r] < 0) continue;
         const int pos = hist[bins[r]] + ranks[r];
-        if (pos < p.n_samples) p.records[pos] = smps[r];  // always true when counts and cursor agree
+        if (pos < p.n_samples) records[pos] = rec[r];  // always true when counts and cursor agree
     }
 }
 
 // ---------------------------------------------------------------- 4. fold
 
 __device__ __forceinline__ int lane_i(int v, int r) { return __builtin_amdgcn_readlane(v, r); }
-__device__ __forceinline__ float lane_f(float v, int r) {
-    return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), r));
-}
 
 constexpr int kFoldBatch = 64;  // records described by one wave at a time (one per lane)
 
@@ -344,7 +353,6 @@ __global__ __launch_bounds__(256) void fold_kernel(Params p, int tile_floats) {
     const int total = p.tile_chunks[p.n_tiles];
     const int nwaves = gridDim.x * kAccWaves;
     const T* gout = static_cast<const T*>(p.grad_out);
-    const float2* loc = reinterpret_cast<const float2*>(p.loc);
     const int half = lane >> 5, slot = lane & 31;
     const int D = DC > 0 ? DC : p.D;
 
@@ -368,7 +376,6 @@ __global__ __launch_bounds__(256) void fold_kernel(Params p, int tile_floats) {
         const int ty = rel / txn, tx = rel - ty * txn;
         const int h_org = ty << th, w_org = tx << tw;
         const int st = __builtin_amdgcn_readfirstlane(s_geo[6 * kMaxLevels + l]);
-        const float Hf = (float)H, Wf = (float)W;
         const TileInfo ti = tile_info(p, s_geo, t);
         const int a0 = p.offsets[ti.own0], a1 = p.offsets[ti.own1];
         const int b0 = ti.l1 > ti.l0 ? p.offsets[ti.l0] : 0, b1 = ti.l1 > ti.l0 ? p.offsets[ti.l1] : 0;
@@ -398,20 +405,17 @@ __global__ __launch_bounds__(256) void fold_kernel(Params p, int tile_floats) {
                 else if ((pos -= na) < nb) idx = b0 + pos;
                 else if ((pos -= nb) < nc) idx = c0 + pos;
                 else idx = d0 + (pos - nc);
-                int smp = p.records[idx < p.n_samples ? idx : 0];
-                smp = smp < 0 || smp >= p.n_samples ? 0 : smp;  // never taken: every slot is filled
-                const int pair = smp / p.K;
-                const float2 xy = loc[smp];
-                const float a = p.attn[smp];
-                const float w_im = __builtin_fmaf(xy.x, Wf, -0.5f);
-                const float h_im = __builtin_fmaf(xy.y, Hf, -0.5f);
+                const int4 rc = reinterpret_cast<const int4*>(p.records)[idx < p.n_samples ? idx : 0];
+                const float a = __builtin_bit_cast(float, rc.y);
+                const float h_im = __builtin_bit_cast(float, rc.z);
+                const float w_im = __builtin_bit_cast(float, rc.w);
                 const float h0f = floorf(h_im), w0f = floorf(w_im);
                 const float lh = h_im - h0f, lw = w_im - w0f;
                 const float hh = 1.f - lh, hw = 1.f - lw;
                 // padded-tile coordinates of the top-left corner, both in [0, T]
                 prow = (int)h0f - h_org + 1;
                 pcol = (int)w0f - w_org + 1;
-                grow = pair * D;
+                grow = rc.x;
                 pk = prow * PW + pcol;
                 w00 = a * (hh * hw);
                 w01 = a * (hh * lw);
@@ -484,10 +488,13 @@ __global__ __launch_bounds__(256) void fold_kernel(Params p, int tile_floats) {
     }
 }
 
-// ---------------------------------------------------------------- 4. fold by gathering (D % 4 == 0)
+// ---------------------------------------------------------------- 4. fold by runs (D % 4 == 0)
 
-constexpr int kTilePix = 64;                    // pixels of an 8x8 tile
-constexpr int kMaxContrib = 4 * kChunkRecords;  // a record adds to at most four pixels of a tile
+constexpr int kRunEdge = 8;                               // tiles of this fold are at most 8 x 8 pixels
+constexpr int kRunPix = kRunEdge * kRunEdge;
+constexpr int kRunKeys = (kRunEdge + 1) * (kRunEdge + 1);  // top-left corner rows / columns -1 .. 7
+constexpr int kGroups = 8;                                 // lane groups per wave (8 lanes, 4 channels each)
+constexpr int kRunBatch = 16;                              // grad_out rows in flight per lane
 
 template <typename T, int VEC>
 struct QuadBuf;
@@ -511,32 +518,77 @@ struct QuadBuf<_Float16, 4> {
     }
 };
 
-// One wave per work item (a tile, or a chunk of a split tile's visible records):
-//   1. every lane describes kChunkRecords/64 records (all their loads in flight together) and
-//      expands each into its contributions to the tile's pixels (corners that fall on the tile
-//      and on the map), counting them per pixel in LDS;
-//   2. a 64-entry scan (one pixel per lane) turns the counts into per-pixel list starts;
-//   3. every contribution (grad_out row, a * corner weight) is placed in its pixel's list;
-//   4. eight lanes serve one pixel (four channels each) and sum its list in registers, sixteen
-//      row reads in flight per lane; reads past a list's end use an out-of-range buffer offset,
-//      which returns zeros, so no lane branches.
-// Each on-map pixel of the tile is stored once (plain store), or added with atomics for split tiles.
+__device__ __forceinline__ void add4(float4& a, float w, const float4& g) {
+    a.x += w * g.x;
+    a.y += w * g.y;
+    a.z += w * g.z;
+    a.w += w * g.w;
+}
+
+struct Corners {
+    float4 v00, v01, v10, v11;
+};
+
+// Adds the four corner sums of the run whose top-left corner has key `key` into the LDS tile
+// (pixels outside the tile belong to neighbouring tiles and are dropped). The corners are
+// written one after another, each read-add-write finished before the next begins: another lane
+// group may be adding the same pixel as a different corner of a different run.
+__device__ __forceinline__ void flush_run(float4* acc, int key, int TH, int TW, int quad, const Corners& c) {
+    const int kr = key / (TW + 1);
+    const int r = kr - 1, col = key - kr * (TW + 1) - 1;
+    auto add_px = [&](int rr, int cc, const float4& v) {
+        if (rr >= 0 && rr < TH && cc >= 0 && cc < TW) {
+            float4* d = acc + (rr * TW + cc) * kGroups + quad;
+            float4 x = *d;
+            x.x += v.x;
+            x.y += v.y;
+            x.z += v.z;
+            x.w += v.w;
+            *d = x;
+        }
+        __asm__ volatile("" ::: "memory");
+    };
+    add_px(r, col, c.v00);
+    add_px(r, col + 1, c.v01);
+    add_px(r + 1, col, c.v10);
+    add_px(r + 1, col + 1, c.v11);
+}
+
+// One wave per work item (a tile, or a chunk of a split tile's visible records), taken from a
+// queue so that a grid of resident workgroups stays busy to the end:
+//   1. every lane loads kChunkRecords/64 records (all loads in flight together) and keys each by
+//      the tile position of its top-left corner; LDS counters rank the records per key;
+//   2. a scan over the keys gives each key's run start, and the records are placed in key order;
+//   3. the sorted records are cut into eight equal slices, one per group of eight lanes (four
+//      channels per lane). A group reads each record's grad_out row once and keeps the current
+//      run's four corner sums in registers; when the key changes the run is added into an LDS
+//      tile. A run that ends inside a slice ends in no other slice, so two groups never add the
+//      same key at once. The run a slice ends on may go on in the next slices: those last runs
+//      are added after the slices are done, one link of each chain of equal keys per round;
+//   4. the tile's on-map pixels are stored once (plain stores), or added with atomics when the
+//      tile is split over several work items (its rows were zeroed before).
+// Every grad_out row read past a slice's end uses an out-of-range buffer offset, which returns zeros.
 template <typename T>
-__global__ __launch_bounds__(256) void fold_gather_kernel(Params p) {
+__global__ __launch_bounds__(256, 2) void fold_runs_kernel(Params p) {
     __shared__ int s_geo[kGeo * kMaxLevels];
-    __shared__ int s_start[kAccWaves][kTilePix + 1];
-    __shared__ int2 s_c[kAccWaves][kMaxContrib];  // (grad_out row, bit pattern of the weight)
+    __shared__ int s_start[kAccWaves][kRunKeys + 1];
+    __shared__ int4 s_rec[kAccWaves][kChunkRecords];        // records sorted by key
+    __shared__ float4 s_acc[kAccWaves][kRunPix * kGroups];  // 32 channels of the tile
     load_geo(p, s_geo);
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
     int* start = s_start[wave];
-    int2* sc = s_c[wave];
+    int4* srec = s_rec[wave];
+    float4* acc = s_acc[wave];
     const int total = p.tile_chunks[p.n_tiles];
-    const int nwaves = gridDim.x * kAccWaves;
     const int D = p.D;
     const rsrc_t gr = make_rsrc(p.grad_out, (uint32_t)((size_t)p.n_batch * p.Lq * p.M * D * sizeof(T)));
-    const int quad = lane & 7, pgrp = lane >> 3;
+    const int quad = lane & 7, grp = lane >> 3;
 
-    for (int item = blockIdx.x * kAccWaves + wave; item < total; item += nwaves) {
+    for (;;) {
+        int next = 0;
+        if (lane == 0) next = atomicAdd(p.queue, 1);
+        const int item = __builtin_amdgcn_readfirstlane(next);
+        if (item >= total) break;
         const int t = __builtin_amdgcn_readfirstlane(p.items[item]);
         if (t < 0 || t >= p.n_tiles) continue;  // never taken: items holds tile indices
         const int first = __builtin_amdgcn_readfirstlane(p.tile_chunks[t]);
@@ -555,9 +607,8 @@ __global__ __launch_bounds__(256) void fold_gather_kernel(Params p) {
         const int ty = rel / txn, tx = rel - ty * txn;
         const int h_org = ty << th, w_org = tx << tw;
         const int st = __builtin_amdgcn_readfirstlane(s_geo[6 * kMaxLevels + l]);
-        const float Hf = (float)H, Wf = (float)W;
-        // pixels of the tile that exist on the map
-        const int th_on = min(TH, H - h_org), tw_on = min(TW, W - w_org);
+        const int th_on = min(TH, H - h_org), tw_on = min(TW, W - w_org);  // tile pixels on the map
+        const int nkeys = (TH + 1) * (TW + 1);
 
         const TileInfo ti = tile_info(p, s_geo, t);
         const int a0 = p.offsets[ti.own0], a1 = p.offsets[ti.own1];
@@ -570,12 +621,11 @@ __global__ __launch_bounds__(256) void fold_gather_kernel(Params p) {
         const int beg = __builtin_amdgcn_readfirstlane(chunk * kChunkRecords);
         const int end = __builtin_amdgcn_readfirstlane(min(beg + kChunkRecords, nvis));
 
-        // 1. describe the records and count their contributions per pixel
+        // 1. load the records and rank them per key
         constexpr int kRecPerLane = kChunkRecords / 64;
-        int rrow[kRecPerLane], rpx[kRecPerLane];  // grad_out row; pixel of corner 00 (tile coords, packed)
-        float4 rw[kRecPerLane];
+        int4 rc[kRecPerLane];
         {
-            int smp[kRecPerLane];
+            const int4* records = reinterpret_cast<const int4*>(p.records);
 #pragma unroll
             for (int i = 0; i < kRecPerLane; ++i) {
                 int pos = beg + i * 64 + lane, idx = -1;
@@ -585,118 +635,146 @@ __global__ __launch_bounds__(256) void fold_gather_kernel(Params p) {
                     else if ((pos -= nb) < nc) idx = c0 + pos;
                     else idx = d0 + (pos - nc);
                 }
-                smp[i] = idx >= 0 && idx < p.n_samples ? p.records[idx] : -1;
-            }
-#pragma unroll
-            for (int i = 0; i < kRecPerLane; ++i) {
-                rpx[i] = -1;
-                if (smp[i] >= 0 && smp[i] < p.n_samples) {
-                    const float2 xy = reinterpret_cast<const float2*>(p.loc)[smp[i]];
-                    const float a = p.attn[smp[i]];
-                    const float w_im = __builtin_fmaf(xy.x, Wf, -0.5f);
-                    const float h_im = __builtin_fmaf(xy.y, Hf, -0.5f);
-                    const float h0f = floorf(h_im), w0f = floorf(w_im);
-                    const float lh = h_im - h0f, lw = w_im - w0f;
-                    const float hh = 1.f - lh, hw = 1.f - lw;
-                    // tile coordinates of corner 00, offset by one so they are >= 0
-                    rpx[i] = (((int)h0f - h_org + 1) << 8) | ((int)w0f - w_org + 1);
-                    rrow[i] = (smp[i] / p.K) * D;
-                    rw[i] = make_float4(a * (hh * hw), a * (hh * lw), a * (lh * hw), a * (lh * lw));
-                }
+                rc[i] = idx >= 0 && idx < p.n_samples ? records[idx] : make_int4(-1, 0, 0, 0);
             }
         }
+        wave_lds_sync();  // the previous item is done with this wave's LDS
+        for (int k = lane; k <= kRunKeys; k += 64) start[k] = 0;
         wave_lds_sync();
-        start[lane] = 0;
-        if (lane == 0) start[kTilePix] = 0;
-        wave_lds_sync();
-        int rank[kRecPerLane][4];
+        int key[kRecPerLane], rank[kRecPerLane];
 #pragma unroll
         for (int i = 0; i < kRecPerLane; ++i) {
-#pragma unroll
-            for (int c = 0; c < 4; ++c) {
-                rank[i][c] = -1;
-                if (rpx[i] >= 0) {
-                    const int pr = (rpx[i] >> 8) - 1 + (c >> 1), pc = (rpx[i] & 0xff) - 1 + (c & 1);
-                    if (pr >= 0 && pr < th_on && pc >= 0 && pc < tw_on) rank[i][c] = atomicAdd(&start[pr * TW + pc], 1);
+            key[i] = -1;
+            rank[i] = 0;
+            if (rc[i].x >= 0) {
+                const float h_im = __builtin_bit_cast(float, rc[i].z);
+                const float w_im = __builtin_bit_cast(float, rc[i].w);
+                const float h0f = floorf(h_im), w0f = floorf(w_im);
+                const int r = (int)h0f - h_org, c = (int)w0f - w_org;
+                // the record keeps (row, a, lh, lw)
+                rc[i].z = __builtin_bit_cast(int, h_im - h0f);
+                rc[i].w = __builtin_bit_cast(int, w_im - w0f);
+                if (r >= -1 && r < TH && c >= -1 && c < TW) {  // always true for a visible record
+                    key[i] = (r + 1) * (TW + 1) + (c + 1);
+                    rank[i] = atomicAdd(&start[key[i]], 1);
                 }
             }
         }
         wave_lds_sync();
-        // 2. per-pixel list starts (one pixel per lane)
-        const int cntp = lane < TH * TW ? start[lane] : 0;
-        int incl = cntp;
-        for (int o = 1; o < 64; o <<= 1) {
-            const int u = __shfl_up(incl, o, 64);
-            if (lane >= o) incl += u;
+        // 2. run starts (two keys per lane) and placement in key order
+        {
+            const int k0 = 2 * lane, k1 = 2 * lane + 1;
+            const int n0 = k0 < nkeys ? start[k0] : 0, n1 = k1 < nkeys ? start[k1] : 0;
+            int incl = n0 + n1;
+            for (int o = 1; o < 64; o <<= 1) {
+                const int u = __shfl_up(incl, o, 64);
+                if (lane >= o) incl += u;
+            }
+            wave_lds_sync();
+            const int excl = incl - n0 - n1;
+            if (k0 < nkeys) start[k0] = excl;
+            if (k1 < nkeys) start[k1] = excl + n0;
+            if (lane == 63) start[nkeys] = incl;
         }
         wave_lds_sync();
-        start[lane] = incl - cntp;
-        if (lane == 63) start[kTilePix] = incl;
-        wave_lds_sync();
-        // 3. place the contributions
 #pragma unroll
         for (int i = 0; i < kRecPerLane; ++i) {
-#pragma unroll
-            for (int c = 0; c < 4; ++c) {
-                if (rank[i][c] >= 0) {
-                    const int pr = (rpx[i] >> 8) - 1 + (c >> 1), pc = (rpx[i] & 0xff) - 1 + (c & 1);
-                    const float wc = c == 0 ? rw[i].x : c == 1 ? rw[i].y : c == 2 ? rw[i].z : rw[i].w;
-                    const int at = start[pr * TW + pc] + rank[i][c];
-                    if (at < kMaxContrib) sc[at] = make_int2(rrow[i], __builtin_bit_cast(int, wc));
-                }
+            if (key[i] >= 0) {
+                const int at = start[key[i]] + rank[i];
+                if (at < kChunkRecords) srec[at] = rc[i];
             }
         }
         wave_lds_sync();
-        // 4. gather: eight lanes per pixel, eight pixels per pass
+
+        // 3. slices of equal length; a slice's first key is the run holding its first record
+        const int C = start[nkeys];
+        const int lo = (C * grp) / kGroups, hi = (C * (grp + 1)) / kGroups;
+        const int span = (C + kGroups - 1) / kGroups;
+        int key_lo = 0;  // last key whose run starts at or before lo
+        for (int stp = 64; stp > 0; stp >>= 1)
+            if (key_lo + stp < nkeys && start[key_lo + stp] <= lo) key_lo += stp;
         const bool split = nitems > 1;
-        for (int px0 = 0; px0 < TH * TW; px0 += 8) {
-            const int px = px0 + pgrp;
-            const bool px_ok = px < TH * TW;
-            const int r = px >> tw, c = px & (TW - 1);
-            const int s0 = px_ok ? start[px] : 0;
-            const int nq = px_ok ? start[px + 1] - s0 : 0;
-            int nmax = nq;
-            for (int o = 32; o > 0; o >>= 1) nmax = max(nmax, __shfl_xor(nmax, o, 64));
-            const int h = h_org + r, w = w_org + c;
-            for (int ch0 = 0; ch0 < D; ch0 += 32) {
-                const int ch = ch0 + 4 * quad;
-                const bool ch_ok = ch < D;
-                float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-                constexpr int kU = 16;
-                for (int j0 = 0; j0 < nmax; j0 += kU) {
-                    float wt[kU];
-                    uint32_t off[kU];
+        for (int ch0 = 0; ch0 < D; ch0 += 4 * kGroups) {
+            const int ch = ch0 + 4 * quad;
+            const bool ch_ok = ch < D;
+            for (int e = lane; e < kRunPix * kGroups; e += 64) acc[e] = make_float4(0.f, 0.f, 0.f, 0.f);
+            wave_lds_sync();
+            int cur = key_lo, bound = start[key_lo + 1];
+            Corners run = {};
+            for (int b = 0; b < span; b += kRunBatch) {
+                uint32_t off[kRunBatch];
+                float ra[kRunBatch], rlh[kRunBatch], rlw[kRunBatch];
 #pragma unroll
-                    for (int u = 0; u < kU; ++u) {
-                        const int j = j0 + u;
-                        const bool act = j < nq && ch_ok;
-                        const int2 e = sc[act ? s0 + j : 0];
-                        wt[u] = act ? __builtin_bit_cast(float, e.y) : 0.f;
-                        off[u] = act ? (uint32_t)(e.x + ch) : (uint32_t)kOOBElem;  // zeros past the list
-                    }
-                    float4 g[kU];
-#pragma unroll
-                    for (int u = 0; u < kU; ++u) g[u] = QuadBuf<T, 4>::load(gr, off[u]);
-#pragma unroll
-                    for (int u = 0; u < kU; ++u) {
-                        acc.x += wt[u] * g[u].x;
-                        acc.y += wt[u] * g[u].y;
-                        acc.z += wt[u] * g[u].z;
-                        acc.w += wt[u] * g[u].w;
-                    }
+                for (int u = 0; u < kRunBatch; ++u) {
+                    const int pos = lo + b + u;
+                    const bool act = pos < hi;
+                    const int4 e = srec[act ? pos : 0];
+                    off[u] = act && ch_ok ? (uint32_t)(e.x + ch) : (uint32_t)kOOBElem;
+                    ra[u] = act ? __builtin_bit_cast(float, e.y) : 0.f;
+                    rlh[u] = __builtin_bit_cast(float, e.z);
+                    rlw[u] = __builtin_bit_cast(float, e.w);
                 }
-                if (px_ok && ch_ok && r < th_on && c < tw_on) {
-                    float* dst = p.grad_value + ((size_t)(n * p.S + st + h * W + w) * p.M + m) * D + ch;
-                    if (split) {
-                        unsafeAtomicAdd(dst + 0, acc.x);
-                        unsafeAtomicAdd(dst + 1, acc.y);
-                        unsafeAtomicAdd(dst + 2, acc.z);
-                        unsafeAtomicAdd(dst + 3, acc.w);
-                    } else {
-                        *reinterpret_cast<float4*>(dst) = acc;
+                float4 g[kRunBatch];
+#pragma unroll
+                for (int u = 0; u < kRunBatch; ++u) g[u] = QuadBuf<T, 4>::load(gr, off[u]);
+#pragma unroll
+                for (int u = 0; u < kRunBatch; ++u) {
+                    const int pos = lo + b + u;
+                    if (pos < hi) {
+                        if (pos >= bound) {  // the run of key `cur` ends before this record
+                            flush_run(acc, cur, TH, TW, quad, run);
+                            run = Corners{};
+                            ++cur;
+                            while (cur + 1 < nkeys && start[cur + 1] <= pos) ++cur;
+                            bound = start[cur + 1];
+                        }
+                        const float lh = rlh[u], lw = rlw[u], hh = 1.f - lh, hw = 1.f - lw, a = ra[u];
+                        add4(run.v00, a * (hh * hw), g[u]);
+                        add4(run.v01, a * (hh * lw), g[u]);
+                        add4(run.v10, a * (lh * hw), g[u]);
+                        add4(run.v11, a * (lh * lw), g[u]);
                     }
                 }
             }
+            // the runs the slices end on: a key may end several neighbouring slices. Each slice
+            // counts the earlier slices that end on its key; round j adds the sums of the slices
+            // with count j, so no two groups add the same key at once
+            const int last = hi > lo ? cur : -1;
+            int link = 0;
+#pragma unroll
+            for (int j = 0; j < kGroups; ++j) {
+                const int kj = __builtin_amdgcn_readlane(last, 8 * j);
+                link += (j < grp && kj == last) ? 1 : 0;
+            }
+#pragma unroll 1
+            for (int j = 0; j < kGroups; ++j)
+                if (last >= 0 && link == j) flush_run(acc, last, TH, TW, quad, run);
+            wave_lds_sync();
+            // 4. store the tile's on-map pixels
+            if (!split) {
+                for (int e = lane; e < kRunPix * kGroups; e += 64) {
+                    const int px = e / kGroups, q = e - px * kGroups;
+                    const int r = px >> tw, c = px & (TW - 1);
+                    if (px < TH * TW && r < th_on && c < tw_on && ch0 + 4 * q < D) {
+                        float* dst = p.grad_value + ((size_t)(n * p.S + st + (h_org + r) * W + w_org + c) * p.M + m) * D +
+                                     ch0 + 4 * q;
+                        *reinterpret_cast<float4*>(dst) = acc[e];
+                    }
+                }
+            } else {
+                // one channel per lane: the atomics of a wave cover whole rows
+                const float* accf = reinterpret_cast<const float*>(acc);
+                for (int e = lane; e < kRunPix * 4 * kGroups; e += 64) {
+                    const int px = e / (4 * kGroups), cc = e - px * (4 * kGroups);
+                    const int r = px >> tw, c = px & (TW - 1);
+                    if (px < TH * TW && r < th_on && c < tw_on && ch0 + cc < D) {
+                        float* dst = p.grad_value + ((size_t)(n * p.S + st + (h_org + r) * W + w_org + c) * p.M + m) * D +
+                                     ch0 + cc;
+                        unsafeAtomicAdd(dst, accf[e]);
+                    }
+                }
+            }
+            wave_lds_sync();
         }
     }
 }
@@ -706,18 +784,20 @@ __global__ __launch_bounds__(256) void fold_gather_kernel(Params p) {
 // ---------------------------------------------------------------- host side
 
 bool plan_binned(Params& p) {
-    if (p.D > kBinnedMaxD || p.Lq == 0 || p.K > kCountQueries) return false;
+    const bool runs = p.D % 4 == 0;  // the run fold: any D, 8 x 8 tiles, 32 channels at a time
+    if ((!runs && p.D > kBinnedMaxD) || p.Lq == 0 || p.K > kCountQueries) return false;
     // grad_out is read through a buffer resource whose out-of-range offset is kOOBElem
     if ((int64_t)p.n_batch * p.Lq * p.M * p.D >= kMaxLaunchElems) return false;
     // largest square tile (2^e x 2^e pixels) whose accumulator, with its one-pixel margin, fits
-    auto padded = [&](int eh, int ew) { return ((1 << eh) + 2) * ((1 << ew) + 2) * p.D; };
-    if (p.D % 4 != 0 && padded(0, 0) > kTileFloats) return false;
+    auto padded = [&](int eh, int ew) { return runs ? 0 : ((1 << eh) + 2) * ((1 << ew) + 2) * p.D; };
+    auto grows = [&](int eh, int ew) { return runs ? eh <= 3 && ew <= 3 : padded(eh, ew) <= kTileFloats; };
     int e_max = 0;
-    while (e_max < 3 && padded(e_max + 1, e_max + 1) <= kTileFloats) ++e_max;
+    while (e_max < 3 && grows(e_max + 1, e_max + 1)) ++e_max;
     int lh[kMaxLevels], lw[kMaxLevels];
-    const bool gather = p.D % 4 == 0;  // fold_gather_kernel: 8x8 tiles everywhere
     for (int l = 0; l < p.L; ++l) {
-        if (gather) {
+        if (runs) {
+            // the run fold reads every visible record once per tile, so the largest tile (the
+            // fewest records straddling into neighbours) is the cheapest
             lh[l] = lw[l] = 3;
             continue;
         }
@@ -744,7 +824,7 @@ bool plan_binned(Params& p) {
         int best = -1;
         int64_t most = 0;
         for (int l = 0; l < p.L; ++l)
-            if (padded(lh[l] + (lh[l] <= lw[l]), lw[l] + (lh[l] > lw[l])) <= kTileFloats && tiles_of(l) > most) {
+            if (grows(lh[l] + (lh[l] <= lw[l]), lw[l] + (lh[l] > lw[l])) && tiles_of(l) > most) {
                 most = tiles_of(l);
                 best = l;
             }
@@ -782,20 +862,39 @@ bool plan_binned(Params& p) {
 
 namespace {
 size_t align256(size_t x) { return (x + 255) / 256 * 256; }
+
+// Workgroups to launch for a queue-driven kernel: four per CU, at least as many as can be resident
+// (the fold's LDS allows two per CU). Workgroups that start after the queue has drained exit at once.
+int queue_grid() {
+    constexpr int kDevs = 64;
+    static std::atomic<int> cache[kDevs];
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return -1;
+    if (dev >= 0 && dev < kDevs) {
+        const int c = cache[dev].load(std::memory_order_relaxed);
+        if (c > 0) return c;
+    }
+    int cus = 0;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return -1;
+    const int grid = 4 * cus;
+    if (dev >= 0 && dev < kDevs && grid > 0) cache[dev].store(grid, std::memory_order_relaxed);
+    return grid;
+}
 }  // namespace
 
 size_t binned_workspace_bytes(const Params& p) {
     const size_t nb = (size_t)p.n_tiles * 4;
-    return align256(nb * 4) + align256((nb + 1) * 4) + align256(nb * 4) + align256(((size_t)p.n_tiles + 1) * 4) +
+    return align256((nb + 1) * 4) + align256((nb + 1) * 4) + align256(nb * 4) + align256(((size_t)p.n_tiles + 1) * 4) +
            align256((size_t)p.max_items * 4) + align256((size_t)p.scan_blocks * 2 * 4) +
-           align256((size_t)p.n_samples * 4);
+           align256((size_t)p.n_samples * 16);
 }
 
 void bind_workspace(Params& p, void* ws) {
     char* c = static_cast<char*>(ws);
     const size_t nb = (size_t)p.n_tiles * 4;
     p.counts = reinterpret_cast<int*>(c);
-    c += align256(nb * 4);
+    p.queue = p.counts + nb;
+    c += align256((nb + 1) * 4);
     p.offsets = reinterpret_cast<int*>(c);
     c += align256((nb + 1) * 4);
     p.cursor = reinterpret_cast<int*>(c);
@@ -811,7 +910,7 @@ void bind_workspace(Params& p, void* ws) {
 
 hipError_t launch_backward_value_binned(const Params& p0, msda_dtype_t dtype, hipStream_t stream) {
     Params p = p0;
-    hipError_t e = launch_zero(reinterpret_cast<float*>(p.counts), (int64_t)p.n_tiles * 4, stream);
+    hipError_t e = launch_zero(reinterpret_cast<float*>(p.counts), (int64_t)p.n_tiles * 4 + 1, stream);
     if (e != hipSuccess) return e;
     p.q_per_block = kCountQueries / p.K > 0 ? kCountQueries / p.K : 1;
     p.chunks = (p.Lq + p.q_per_block - 1) / p.q_per_block;
@@ -829,20 +928,22 @@ hipError_t launch_backward_value_binned(const Params& p0, msda_dtype_t dtype, hi
     if ((e = hipGetLastError()) != hipSuccess) return e;
     hipLaunchKernelGGL(bin_scatter_kernel, dim3(bin_blocks), dim3(256), hist_lds, stream, p);
     if ((e = hipGetLastError()) != hipSuccess) return e;
+    if (p.D % 4 == 0) {
+        const int grid = queue_grid();  // the waves take work items from the queue
+        if (grid <= 0) return hipErrorInvalidConfiguration;
+        if (dtype == MSDA_F16)
+            hipLaunchKernelGGL(fold_runs_kernel<_Float16>, dim3(grid), dim3(256), 0, stream, p);
+        else
+            hipLaunchKernelGGL(fold_runs_kernel<float>, dim3(grid), dim3(256), 0, stream, p);
+        return hipGetLastError();
+    }
     int tile_floats = 0;
     for (int l = 0; l < p.L; ++l) {
         const int f = ((1 << p.tile_lh[l]) + 2) * ((1 << p.tile_lw[l]) + 2) * p.D;
         if (f > tile_floats) tile_floats = f;
     }
     const size_t lds = (size_t)kAccWaves * tile_floats * sizeof(float);
-    const int fold_blocks = 768;  // three workgroups per CU are resident (LDS-bound)
-    if (p.D % 4 == 0) {
-        if (dtype == MSDA_F16)
-            hipLaunchKernelGGL(fold_gather_kernel<_Float16>, dim3(fold_blocks), dim3(256), 0, stream, p);
-        else
-            hipLaunchKernelGGL(fold_gather_kernel<float>, dim3(fold_blocks), dim3(256), 0, stream, p);
-        return hipGetLastError();
-    }
+    const int fold_blocks = 768;
     const bool d32 = p.D == 32;
     if (dtype == MSDA_F16) {
         if (d32) hipLaunchKernelGGL((fold_kernel<_Float16, 32>), dim3(fold_blocks), dim3(256), lds, stream, p, tile_floats);

@@ -55,12 +55,13 @@ struct Params {
     int max_items;              // capacity of `items`
     int scan_blocks;            // ceil(n_tiles / kScanTiles)
     int* counts;                // [n_tiles * 4]       samples per (tile, class)
+    int* queue;                 // [1]                 next work item of the fold (zeroed with counts)
     int* offsets;               // [n_tiles * 4 + 1]   exclusive prefix of counts
     int* cursor;                // [n_tiles * 4]       fill position per bin
     int* tile_chunks;           // [n_tiles + 1]       exclusive prefix of work items per tile
     int* items;                 // [max_items]         work item -> tile
     int* block_sums;            // [2 * scan_blocks]
-    int* records;               // [n_samples]         launch-local sample index, sorted by bin
+    int* records;               // [n_samples][4]      {grad_out row, a, h_im, w_im} per sample, sorted by bin
 };
 
 hipError_t launch_forward(const Params& p, msda_dtype_t dtype, hipStream_t stream);
