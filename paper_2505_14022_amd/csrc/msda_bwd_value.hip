@@ -248,14 +248,19 @@ __global__ __launch_bounds__(256) void scan_apply_kernel(Params p) {
     }
 }
 
-// Rows of tiles that are folded by several work items start at zero (they are added to).
-__global__ __launch_bounds__(256) void zero_split_kernel(Params p) {
+// Per tile (one wave): the descriptors of its work items for the fold, and zeroed grad_value rows
+// when the tile is folded by several work items (they add their sums).
+//   descriptor: {beg, end, split, level, n, m, h_org, w_org, own start, own count, left start,
+//                left count, up start, up count, up-left start, 0}: the item folds visible records
+//                [beg, end) of the tile, counted through the own / left / up / up-left bin ranges
+__global__ __launch_bounds__(256) void prep_items_kernel(Params p) {
     __shared__ int s_geo[kGeo * kMaxLevels];
     load_geo(p, s_geo);
     const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
     const int lane = threadIdx.x & 63;
     if (t >= p.n_tiles) return;
-    if (p.tile_chunks[t + 1] - p.tile_chunks[t] <= 1) return;
+    const int first = p.tile_chunks[t];
+    const int nit = p.tile_chunks[t + 1] - first;
     const int slab = t / p.tiles_per_slab, tin = t - slab * p.tiles_per_slab;
     const int n = slab / p.M, m = slab - n * p.M;
     const int l = level_of_tile(s_geo, p.L, tin);
@@ -264,10 +269,26 @@ __global__ __launch_bounds__(256) void zero_split_kernel(Params p) {
     const int rel = tin - s_geo[5 * kMaxLevels + l], txn = s_geo[4 * kMaxLevels + l];
     const int ty = rel / txn, tx = rel - ty * txn;
     const int st = s_geo[6 * kMaxLevels + l];
+    const int h_org = ty << th, w_org = tx << tw;
+    const TileInfo ti = tile_info(p, s_geo, t);
+    const int a0 = p.offsets[ti.own0], na = p.offsets[ti.own1] - a0;
+    const int b0 = ti.l1 > ti.l0 ? p.offsets[ti.l0] : 0, nb = ti.l1 > ti.l0 ? p.offsets[ti.l1] - b0 : 0;
+    const int c0 = ti.u1 > ti.u0 ? p.offsets[ti.u0] : 0, nc = ti.u1 > ti.u0 ? p.offsets[ti.u1] - c0 : 0;
+    const int d0 = ti.d1 > ti.d0 ? p.offsets[ti.d0] : 0, nd = ti.d1 > ti.d0 ? p.offsets[ti.d1] - d0 : 0;
+    const int nvis = na + nb + nc + nd;
+    for (int c = lane; c < nit && first + c < p.max_items; c += 64) {
+        int4* d = reinterpret_cast<int4*>(p.item_desc) + (size_t)(first + c) * 4;
+        const int beg = c * kChunkRecords;
+        d[0] = make_int4(beg, min(beg + kChunkRecords, nvis), nit > 1, l);
+        d[1] = make_int4(n, m, h_org, w_org);
+        d[2] = make_int4(a0, na, b0, nb);
+        d[3] = make_int4(c0, nc, d0, 0);
+    }
+    if (nit <= 1) return;
     const int npx = 1 << (th + tw);
     for (int e = lane; e < npx * p.D; e += 64) {
         const int px = e / p.D, ch = e - px * p.D;
-        const int h = (ty << th) + (px >> tw), w = (tx << tw) + (px & ((1 << tw) - 1));
+        const int h = h_org + (px >> tw), w = w_org + (px & ((1 << tw) - 1));
         if (h < H && w < W) p.grad_value[((size_t)(n * p.S + st + h * W + w) * p.M + m) * p.D + ch] = 0.f;
     }
 }
@@ -492,7 +513,11 @@ __global__ __launch_bounds__(256) void fold_kernel(Params p, int tile_floats) {
 
 constexpr int kRunEdge = 8;                               // tiles of this fold are at most 8 x 8 pixels
 constexpr int kRunPix = kRunEdge * kRunEdge;
-constexpr int kRunKeys = (kRunEdge + 1) * (kRunEdge + 1);  // top-left corner rows / columns -1 .. 7
+// key of a record: the tile position of its top-left corner (rows and columns -1 .. 7), one key
+// row per 16 keys so that keys ascend in raster order and decode with shifts
+constexpr int kKeyShift = 4;
+constexpr int kRunKeys = (kRunEdge + 1) << kKeyShift;
+constexpr int kKeysPerLane = (kRunKeys + 63) / 64;
 constexpr int kGroups = 8;                                 // lane groups per wave (8 lanes, 4 channels each)
 constexpr int kRunBatch = 16;                              // grad_out rows in flight per lane
 
@@ -534,8 +559,7 @@ struct Corners {
 // written one after another, each read-add-write finished before the next begins: another lane
 // group may be adding the same pixel as a different corner of a different run.
 __device__ __forceinline__ void flush_run(float4* acc, int key, int TH, int TW, int quad, const Corners& c) {
-    const int kr = key / (TW + 1);
-    const int r = kr - 1, col = key - kr * (TW + 1) - 1;
+    const int r = (key >> kKeyShift) - 1, col = (key & ((1 << kKeyShift) - 1)) - 1;
     auto add_px = [&](int rr, int cc, const float4& v) {
         if (rr >= 0 && rr < TH && cc >= 0 && cc < TW) {
             float4* d = acc + (rr * TW + cc) * kGroups + quad;
@@ -579,47 +603,42 @@ __global__ __launch_bounds__(256, 2) void fold_runs_kernel(Params p) {
     int* start = s_start[wave];
     int4* srec = s_rec[wave];
     float4* acc = s_acc[wave];
-    const int total = p.tile_chunks[p.n_tiles];
     const int D = p.D;
     const rsrc_t gr = make_rsrc(p.grad_out, (uint32_t)((size_t)p.n_batch * p.Lq * p.M * D * sizeof(T)));
     const int quad = lane & 7, grp = lane >> 3;
 
+    // Work items come from one queue in slab-major order, so the waves in flight at any time work
+    // on neighbouring tiles of a few slabs, spread over all XCDs. (Giving each XCD slabs of its
+    // own was slower: one head's rows lie 1 KB apart in the interleaved layouts, so an XCD working
+    // on a single head keeps few L2 channels busy.)
+    const int total = p.tile_chunks[p.n_tiles];
+    int taken = 0;
+    if (lane == 0) taken = atomicAdd(p.queue, 1);
     for (;;) {
-        int next = 0;
-        if (lane == 0) next = atomicAdd(p.queue, 1);
-        const int item = __builtin_amdgcn_readfirstlane(next);
+        const int item = __builtin_amdgcn_readfirstlane(taken);
         if (item >= total) break;
-        const int t = __builtin_amdgcn_readfirstlane(p.items[item]);
-        if (t < 0 || t >= p.n_tiles) continue;  // never taken: items holds tile indices
-        const int first = __builtin_amdgcn_readfirstlane(p.tile_chunks[t]);
-        const int nitems = __builtin_amdgcn_readfirstlane(p.tile_chunks[t + 1]) - first;
-        const int chunk = item - first;
-        const int slab = t / p.tiles_per_slab, tin = t - slab * p.tiles_per_slab;
-        const int n = slab / p.M, m = slab - n * p.M;
-        const int l = __builtin_amdgcn_readfirstlane(level_of_tile(s_geo, p.L, tin));
+        // the next item is taken now; it is needed only when this one is done
+        if (lane == 0) taken = atomicAdd(p.queue, 1);
+        int dv = 0;
+        if (lane < 16) dv = p.item_desc[(size_t)item * 16 + lane];
+        const int beg = __builtin_amdgcn_readlane(dv, 0), end = __builtin_amdgcn_readlane(dv, 1);
+        const bool split = __builtin_amdgcn_readlane(dv, 2) != 0;
+        const int l = __builtin_amdgcn_readlane(dv, 3);
+        const int n = __builtin_amdgcn_readlane(dv, 4), m = __builtin_amdgcn_readlane(dv, 5);
+        const int h_org = __builtin_amdgcn_readlane(dv, 6), w_org = __builtin_amdgcn_readlane(dv, 7);
+        const int a0 = __builtin_amdgcn_readlane(dv, 8), na = __builtin_amdgcn_readlane(dv, 9);
+        const int b0 = __builtin_amdgcn_readlane(dv, 10), nb = __builtin_amdgcn_readlane(dv, 11);
+        const int c0 = __builtin_amdgcn_readlane(dv, 12), nc = __builtin_amdgcn_readlane(dv, 13);
+        const int d0 = __builtin_amdgcn_readlane(dv, 14);
+        if (l < 0 || l >= p.L) continue;  // never taken: descriptors name a level of the map
         const int H = __builtin_amdgcn_readfirstlane(s_geo[l]);
         const int W = __builtin_amdgcn_readfirstlane(s_geo[kMaxLevels + l]);
         const int th = __builtin_amdgcn_readfirstlane(s_geo[2 * kMaxLevels + l]);
         const int tw = __builtin_amdgcn_readfirstlane(s_geo[3 * kMaxLevels + l]);
         const int TH = 1 << th, TW = 1 << tw;
-        const int rel = tin - __builtin_amdgcn_readfirstlane(s_geo[5 * kMaxLevels + l]);
-        const int txn = __builtin_amdgcn_readfirstlane(s_geo[4 * kMaxLevels + l]);
-        const int ty = rel / txn, tx = rel - ty * txn;
-        const int h_org = ty << th, w_org = tx << tw;
         const int st = __builtin_amdgcn_readfirstlane(s_geo[6 * kMaxLevels + l]);
         const int th_on = min(TH, H - h_org), tw_on = min(TW, W - w_org);  // tile pixels on the map
-        const int nkeys = (TH + 1) * (TW + 1);
-
-        const TileInfo ti = tile_info(p, s_geo, t);
-        const int a0 = p.offsets[ti.own0], a1 = p.offsets[ti.own1];
-        const int b0 = ti.l1 > ti.l0 ? p.offsets[ti.l0] : 0, b1 = ti.l1 > ti.l0 ? p.offsets[ti.l1] : 0;
-        const int c0 = ti.u1 > ti.u0 ? p.offsets[ti.u0] : 0, c1 = ti.u1 > ti.u0 ? p.offsets[ti.u1] : 0;
-        const int d0 = ti.d1 > ti.d0 ? p.offsets[ti.d0] : 0, d1 = ti.d1 > ti.d0 ? p.offsets[ti.d1] : 0;
-        const int na = __builtin_amdgcn_readfirstlane(a1 - a0), nb = __builtin_amdgcn_readfirstlane(b1 - b0);
-        const int nc = __builtin_amdgcn_readfirstlane(c1 - c0), nd = __builtin_amdgcn_readfirstlane(d1 - d0);
-        const int nvis = na + nb + nc + nd;
-        const int beg = __builtin_amdgcn_readfirstlane(chunk * kChunkRecords);
-        const int end = __builtin_amdgcn_readfirstlane(min(beg + kChunkRecords, nvis));
+        const int nkeys = (TH + 1) << kKeyShift;
 
         // 1. load the records and rank them per key
         constexpr int kRecPerLane = kChunkRecords / 64;
@@ -647,33 +666,37 @@ __global__ __launch_bounds__(256, 2) void fold_runs_kernel(Params p) {
             key[i] = -1;
             rank[i] = 0;
             if (rc[i].x >= 0) {
-                const float h_im = __builtin_bit_cast(float, rc[i].z);
-                const float w_im = __builtin_bit_cast(float, rc[i].w);
-                const float h0f = floorf(h_im), w0f = floorf(w_im);
-                const int r = (int)h0f - h_org, c = (int)w0f - w_org;
-                // the record keeps (row, a, lh, lw)
-                rc[i].z = __builtin_bit_cast(int, h_im - h0f);
-                rc[i].w = __builtin_bit_cast(int, w_im - w0f);
+                const int r = (int)floorf(__builtin_bit_cast(float, rc[i].z)) - h_org;
+                const int c = (int)floorf(__builtin_bit_cast(float, rc[i].w)) - w_org;
                 if (r >= -1 && r < TH && c >= -1 && c < TW) {  // always true for a visible record
-                    key[i] = (r + 1) * (TW + 1) + (c + 1);
+                    key[i] = ((r + 1) << kKeyShift) + c + 1;
                     rank[i] = atomicAdd(&start[key[i]], 1);
                 }
             }
         }
         wave_lds_sync();
-        // 2. run starts (two keys per lane) and placement in key order
+        // 2. run starts (kKeysPerLane consecutive keys per lane) and placement in key order
         {
-            const int k0 = 2 * lane, k1 = 2 * lane + 1;
-            const int n0 = k0 < nkeys ? start[k0] : 0, n1 = k1 < nkeys ? start[k1] : 0;
-            int incl = n0 + n1;
+            int cnt[kKeysPerLane], sum = 0;
+#pragma unroll
+            for (int j = 0; j < kKeysPerLane; ++j) {
+                const int k = kKeysPerLane * lane + j;
+                cnt[j] = k < nkeys ? start[k] : 0;
+                sum += cnt[j];
+            }
+            int incl = sum;
             for (int o = 1; o < 64; o <<= 1) {
                 const int u = __shfl_up(incl, o, 64);
                 if (lane >= o) incl += u;
             }
             wave_lds_sync();
-            const int excl = incl - n0 - n1;
-            if (k0 < nkeys) start[k0] = excl;
-            if (k1 < nkeys) start[k1] = excl + n0;
+            int run_start = incl - sum;
+#pragma unroll
+            for (int j = 0; j < kKeysPerLane; ++j) {
+                const int k = kKeysPerLane * lane + j;
+                if (k < nkeys) start[k] = run_start;
+                run_start += cnt[j];
+            }
             if (lane == 63) start[nkeys] = incl;
         }
         wave_lds_sync();
@@ -686,24 +709,28 @@ __global__ __launch_bounds__(256, 2) void fold_runs_kernel(Params p) {
         }
         wave_lds_sync();
 
-        // 3. slices of equal length; a slice's first key is the run holding its first record
+        // 3. slices of equal length
         const int C = start[nkeys];
         const int lo = (C * grp) / kGroups, hi = (C * (grp + 1)) / kGroups;
         const int span = (C + kGroups - 1) / kGroups;
-        int key_lo = 0;  // last key whose run starts at or before lo
-        for (int stp = 64; stp > 0; stp >>= 1)
-            if (key_lo + stp < nkeys && start[key_lo + stp] <= lo) key_lo += stp;
-        const bool split = nitems > 1;
+        auto key_of = [&](float h0f, float w0f) {
+            return (((int)h0f - h_org + 1) << kKeyShift) + ((int)w0f - w_org + 1);
+        };
+        int key_lo = 0;  // key of the slice's first record
+        if (hi > lo) {
+            const int4 e = srec[lo];
+            key_lo = key_of(floorf(__builtin_bit_cast(float, e.z)), floorf(__builtin_bit_cast(float, e.w)));
+        }
         for (int ch0 = 0; ch0 < D; ch0 += 4 * kGroups) {
             const int ch = ch0 + 4 * quad;
             const bool ch_ok = ch < D;
             for (int e = lane; e < kRunPix * kGroups; e += 64) acc[e] = make_float4(0.f, 0.f, 0.f, 0.f);
             wave_lds_sync();
-            int cur = key_lo, bound = start[key_lo + 1];
+            int cur = key_lo;
             Corners run = {};
             for (int b = 0; b < span; b += kRunBatch) {
                 uint32_t off[kRunBatch];
-                float ra[kRunBatch], rlh[kRunBatch], rlw[kRunBatch];
+                float ra[kRunBatch], rh[kRunBatch], rw[kRunBatch];
 #pragma unroll
                 for (int u = 0; u < kRunBatch; ++u) {
                     const int pos = lo + b + u;
@@ -711,8 +738,8 @@ __global__ __launch_bounds__(256, 2) void fold_runs_kernel(Params p) {
                     const int4 e = srec[act ? pos : 0];
                     off[u] = act && ch_ok ? (uint32_t)(e.x + ch) : (uint32_t)kOOBElem;
                     ra[u] = act ? __builtin_bit_cast(float, e.y) : 0.f;
-                    rlh[u] = __builtin_bit_cast(float, e.z);
-                    rlw[u] = __builtin_bit_cast(float, e.w);
+                    rh[u] = __builtin_bit_cast(float, e.z);
+                    rw[u] = __builtin_bit_cast(float, e.w);
                 }
                 float4 g[kRunBatch];
 #pragma unroll
@@ -721,14 +748,14 @@ __global__ __launch_bounds__(256, 2) void fold_runs_kernel(Params p) {
                 for (int u = 0; u < kRunBatch; ++u) {
                     const int pos = lo + b + u;
                     if (pos < hi) {
-                        if (pos >= bound) {  // the run of key `cur` ends before this record
+                        const float h0f = floorf(rh[u]), w0f = floorf(rw[u]);
+                        const int key = key_of(h0f, w0f);
+                        if (key != cur) {  // the run of key `cur` ends before this record
                             flush_run(acc, cur, TH, TW, quad, run);
                             run = Corners{};
-                            ++cur;
-                            while (cur + 1 < nkeys && start[cur + 1] <= pos) ++cur;
-                            bound = start[cur + 1];
+                            cur = key;
                         }
-                        const float lh = rlh[u], lw = rlw[u], hh = 1.f - lh, hw = 1.f - lw, a = ra[u];
+                        const float lh = rh[u] - h0f, lw = rw[u] - w0f, hh = 1.f - lh, hw = 1.f - lw, a = ra[u];
                         add4(run.v00, a * (hh * hw), g[u]);
                         add4(run.v01, a * (hh * lw), g[u]);
                         add4(run.v10, a * (lh * hw), g[u]);
@@ -884,7 +911,8 @@ int queue_grid() {
 
 size_t binned_workspace_bytes(const Params& p) {
     const size_t nb = (size_t)p.n_tiles * 4;
-    return align256((nb + 1) * 4) + align256((nb + 1) * 4) + align256(nb * 4) + align256(((size_t)p.n_tiles + 1) * 4) +
+    return align256((nb + 1) * 4) + align256((size_t)p.max_items * 64) + align256((nb + 1) * 4) + align256(nb * 4) +
+           align256(((size_t)p.n_tiles + 1) * 4) +
            align256((size_t)p.max_items * 4) + align256((size_t)p.scan_blocks * 2 * 4) +
            align256((size_t)p.n_samples * 16);
 }
@@ -895,6 +923,8 @@ void bind_workspace(Params& p, void* ws) {
     p.counts = reinterpret_cast<int*>(c);
     p.queue = p.counts + nb;
     c += align256((nb + 1) * 4);
+    p.item_desc = reinterpret_cast<int*>(c);
+    c += align256((size_t)p.max_items * 64);
     p.offsets = reinterpret_cast<int*>(c);
     c += align256((nb + 1) * 4);
     p.cursor = reinterpret_cast<int*>(c);
@@ -924,7 +954,7 @@ hipError_t launch_backward_value_binned(const Params& p0, msda_dtype_t dtype, hi
     if ((e = hipGetLastError()) != hipSuccess) return e;
     hipLaunchKernelGGL(scan_apply_kernel, dim3(p.scan_blocks), dim3(256), 0, stream, p);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    hipLaunchKernelGGL(zero_split_kernel, dim3((p.n_tiles + 3) / 4), dim3(256), 0, stream, p);
+    hipLaunchKernelGGL(prep_items_kernel, dim3((p.n_tiles + 3) / 4), dim3(256), 0, stream, p);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     hipLaunchKernelGGL(bin_scatter_kernel, dim3(bin_blocks), dim3(256), hist_lds, stream, p);
     if ((e = hipGetLastError()) != hipSuccess) return e;

@@ -56,6 +56,7 @@ struct Params {
     int scan_blocks;            // ceil(n_tiles / kScanTiles)
     int* counts;                // [n_tiles * 4]       samples per (tile, class)
     int* queue;                 // [1]                 next work item of the fold (zeroed with counts)
+    int* item_desc;             // [max_items * 16]    fold work item descriptors
     int* offsets;               // [n_tiles * 4 + 1]   exclusive prefix of counts
     int* cursor;                // [n_tiles * 4]       fill position per bin
     int* tile_chunks;           // [n_tiles + 1]       exclusive prefix of work items per tile
