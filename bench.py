@@ -155,6 +155,8 @@ def main():
     ap.add_argument("--workload", default="detr_encoder", choices=sorted(workloads.BY_NAME))
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-compulsory", action="store_true", help="skip counting touched rows (faster)")
+    ap.add_argument("--atomic-grad-value", action="store_true",
+                    help="pass no workspace, so msda_backward accumulates grad_value with fp32 atomics")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="instead of the benchmark, copy a MIB-mebibyte fp32 buffer 5 times (a plain copy kernel of "
                          "known size, used to scale FETCH_SIZE / WRITE_SIZE counters)")
@@ -198,7 +200,7 @@ def main():
     dt = msda.MSDA_F16 if w.dtype == "f16" else msda.MSDA_F32
     shapes = np.ascontiguousarray(inp.shapes.reshape(-1))
     starts = np.ascontiguousarray(inp.starts)
-    ws_bytes = msda.workspace_size(inp.shapes, inp.starts, *dims, dt)
+    ws_bytes = 0 if args.atomic_grad_value else msda.workspace_size(inp.shapes, inp.starts, *dims, dt)
     ws = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device=dev)
     P_ = (value.data_ptr(), loc.data_ptr(), attn.data_ptr(), gout.data_ptr(), out.data_ptr(), gv.data_ptr(),
           gl.data_ptr(), ga.data_ptr(), ws.data_ptr() if ws_bytes else None)

@@ -95,12 +95,14 @@ msda_status_t msda_forward(const void* value, const int64_t* spatial_shapes,
  * At an integer h_im (or w_im) the location gradient is the one of the cell [floor, floor+1];
  * samples outside the open range above get zero location and weight gradients.
  *
- * workspace: DEVICE scratch of at least the size msda_backward_workspace_size() reports, 256-byte
- * aligned, owned by the caller and not used by anything else until the enqueued work completes.
- * With a workspace, grad_value is computed owner-by-owner: samples are sorted by the pixel tile
- * they touch and each grad_value row is written once by the wave that owns its tile. With
- * workspace == NULL, grad_value is zeroed and accumulated with fp32 atomics (slower). A non-null
- * workspace smaller than required is an error.
+ * workspace: DEVICE scratch of at least the size msda_backward_workspace_size(...,
+ * MSDA_WORKSPACE_OWNER, ...) reports, 256-byte aligned, owned by the caller and not used by
+ * anything else until the enqueued work completes. With a workspace, grad_value is computed
+ * owner-by-owner: samples are sorted by the pixel tile they touch and each grad_value row is
+ * written once by the wave that owns its tile (rows of tiles seen by more than one chunk of 512
+ * samples are added with atomics). With workspace == NULL, or when the owner-computes path does
+ * not apply, grad_value is zeroed and accumulated with fp32 atomics. A non-null workspace smaller
+ * than required is an error.
  *
  * value and grad_out 16-byte aligned; grad_value 16-byte; grad_loc 8-byte; grad_attn 4-byte.
  * N*Lq == 0 still zeroes grad_value.
@@ -112,15 +114,22 @@ msda_status_t msda_backward(const void* value, const int64_t* spatial_shapes,
                             int64_t N, int64_t S, int64_t M, int64_t D, int64_t Lq, int64_t L,
                             int64_t P, int dtype, void* stream);
 
+/* Modes of msda_backward_workspace_size. */
+#define MSDA_WORKSPACE_PREFERRED 0 /* the workspace the library would use: 0 bytes where fp32 atomics
+                                      are expected to be faster (fewer than one sample per two value
+                                      rows, or at most 16384 samples)                               */
+#define MSDA_WORKSPACE_OWNER 1     /* the owner-computes workspace whenever that path applies      */
+
 /*
- * Workspace bytes msda_backward needs for this problem to take the owner-computes grad_value
- * path (host-only; checks the problem like msda_check_args). *bytes is 0 when that path does not
- * apply (D > 64, more than 16384 tile bins per (batch, head) slab, or an empty problem); then
- * msda_backward ignores the workspace and uses atomics.
+ * Workspace bytes for msda_backward (host-only; checks the problem like msda_check_args; an
+ * unknown mode is MSDA_ERROR_INVALID_VALUE). *bytes is 0 when the owner-computes grad_value path
+ * does not apply (D % 4 != 0 with D > 355, more than 15872 tile bins per (batch, head) slab,
+ * index ranges beyond 2^31, or an empty problem) or, in MSDA_WORKSPACE_PREFERRED mode, when atomics
+ * are preferred; then msda_backward is called without a workspace.
  */
 msda_status_t msda_backward_workspace_size(const int64_t* spatial_shapes, const int64_t* level_start_index,
                                            int64_t N, int64_t S, int64_t M, int64_t D, int64_t Lq,
-                                           int64_t L, int64_t P, int dtype, size_t* bytes);
+                                           int64_t L, int64_t P, int dtype, int mode, size_t* bytes);
 
 /* Static name of a status code ("MSDA_SUCCESS", ...). */
 const char* msda_status_string(msda_status_t status);

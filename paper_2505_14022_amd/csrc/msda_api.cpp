@@ -136,15 +136,18 @@ msda_status_t msda_forward(const void* value, const int64_t* spatial_shapes, con
 
 msda_status_t msda_backward_workspace_size(const int64_t* spatial_shapes, const int64_t* level_start_index,
                                            int64_t N, int64_t S, int64_t M, int64_t D, int64_t Lq, int64_t L,
-                                           int64_t P, int dtype, size_t* bytes) {
+                                           int64_t P, int dtype, int mode, size_t* bytes) {
     if (!bytes) return fail(MSDA_ERROR_INVALID_VALUE, "bytes must be non-null");
     *bytes = 0;
     msda_status_t st = check_problem(spatial_shapes, level_start_index, N, S, M, D, Lq, L, P, dtype);
     if (st != MSDA_SUCCESS) return st;
+    if (mode != MSDA_WORKSPACE_PREFERRED && mode != MSDA_WORKSPACE_OWNER)
+        return fail(MSDA_ERROR_INVALID_VALUE, "unknown workspace mode %d", mode);
     if (N * Lq == 0) return ok();
     const int64_t nb = batch_per_launch(S, M, D, Lq, L, P);
     msda::Params p = base_params(spatial_shapes, level_start_index, S, M, D, Lq, L, P);
     p.n_batch = (int)(N < nb ? N : nb);
+    if (mode == MSDA_WORKSPACE_PREFERRED && msda::prefer_atomic(p)) return ok();
     if (msda::plan_binned(p)) *bytes = msda::binned_workspace_bytes(p);
     return ok();
 }
@@ -179,7 +182,8 @@ msda_status_t msda_backward(const void* value, const int64_t* spatial_shapes, co
     bool binned = false;
     if (workspace) {
         size_t need = 0;
-        msda_backward_workspace_size(spatial_shapes, level_start_index, N, S, M, D, Lq, L, P, dtype, &need);
+        msda_backward_workspace_size(spatial_shapes, level_start_index, N, S, M, D, Lq, L, P, dtype,
+                                     MSDA_WORKSPACE_OWNER, &need);
         if (need > 0) {
             if (workspace_bytes < need)
                 return fail(MSDA_ERROR_INVALID_VALUE, "workspace of %zu bytes is smaller than the %zu needed",

@@ -70,17 +70,22 @@ __global__ __launch_bounds__(kBlock) void bwd_kernel(Params p) {
                         gw += g[i] * (hh * (v1[i] - v0[i]) + lh * (v3[i] - v2[i]));
                         gh += g[i] * (hw * (v2[i] - v0[i]) + lw * (v3[i] - v1[i]));
                     }
-                    if constexpr (ATOMIC) {
-                        // grad_value[corner] += a * w_corner * g   (fp32 rows)
-                        const uint32_t gcb = (uint32_t)chan << 2;
-                        const float a0 = a * w.x, a1 = a * w.y, a2 = a * w.z, a3 = a * w.w;
+                }
+                if constexpr (ATOMIC) {
+                    // grad_value[corner] += a * w_corner * g (fp32 rows). Lane `sub` adds channels
+                    // c0 + sub + LPP*i, so each atomic instruction covers LPP contiguous floats of
+                    // a row (whole 32- or 64-byte segments) instead of a strided set.
+                    const float a0 = a * w.x, a1 = a * w.y, a2 = a * w.z, a3 = a * w.w;
 #pragma unroll
-                        for (int i = 0; i < VEC; ++i) {
-                            const uint32_t ci = gcb + 4u * i;
-                            __builtin_amdgcn_raw_ptr_buffer_atomic_fadd_f32(a0 * g[i], gr, ((uint32_t)off.x << 2) + ci, 0, 0);
-                            __builtin_amdgcn_raw_ptr_buffer_atomic_fadd_f32(a1 * g[i], gr, ((uint32_t)off.y << 2) + ci, 0, 0);
-                            __builtin_amdgcn_raw_ptr_buffer_atomic_fadd_f32(a2 * g[i], gr, ((uint32_t)off.z << 2) + ci, 0, 0);
-                            __builtin_amdgcn_raw_ptr_buffer_atomic_fadd_f32(a3 * g[i], gr, ((uint32_t)off.w << 2) + ci, 0, 0);
+                    for (int i = 0; i < VEC; ++i) {
+                        const int ct = c0 + sub + LPP * i;
+                        if (ct < p.D) {
+                            const float gt = (float)gout[gout_row + ct];
+                            const uint32_t ci = (uint32_t)ct << 2;
+                            __builtin_amdgcn_raw_ptr_buffer_atomic_fadd_f32(a0 * gt, gr, ((uint32_t)off.x << 2) + ci, 0, 0);
+                            __builtin_amdgcn_raw_ptr_buffer_atomic_fadd_f32(a1 * gt, gr, ((uint32_t)off.y << 2) + ci, 0, 0);
+                            __builtin_amdgcn_raw_ptr_buffer_atomic_fadd_f32(a2 * gt, gr, ((uint32_t)off.z << 2) + ci, 0, 0);
+                            __builtin_amdgcn_raw_ptr_buffer_atomic_fadd_f32(a3 * gt, gr, ((uint32_t)off.w << 2) + ci, 0, 0);
                         }
                     }
                 }

@@ -810,6 +810,17 @@ __global__ __launch_bounds__(256, 2) void fold_runs_kernel(Params p) {
 
 // ---------------------------------------------------------------- host side
 
+bool prefer_atomic(const Params& p) {
+    const int64_t samples = (int64_t)p.n_batch * p.Lq * p.M * p.K;
+    // Below one sample per two value rows the binned path's fixed cost (every tile of every slab is
+    // folded and stored) outweighs the atomics it saves: at the DETR-decoder shape the two paths
+    // break even near 0.8 samples per row, and atomics take 40 % of the binned time at 0.24.
+    if (2 * samples < (int64_t)p.n_batch * p.S * p.M) return true;
+    // Small problems likewise: the binned path's nine launches cost about 80 us at 128 samples, while
+    // atomics from at most 16384 samples take a few microseconds even when they all hit one row.
+    return samples <= kAtomicMaxSamples;
+}
+
 bool plan_binned(Params& p) {
     const bool runs = p.D % 4 == 0;  // the run fold: any D, 8 x 8 tiles, 32 channels at a time
     if ((!runs && p.D > kBinnedMaxD) || p.Lq == 0 || p.K > kCountQueries) return false;

@@ -23,7 +23,8 @@ constexpr int kTileFloats = 3200;    // LDS floats of one tile accumulator with 
 constexpr int kBinnedMaxD = 355;     // channels per head handled by the binned path (1x1 tiles)
 constexpr int kChunkRecords = 512;   // records folded by one accumulate work item
 constexpr int kCountQueries = 4096;  // samples per workgroup in the counting / scatter passes
-constexpr int kScanTiles = 1024;     // tiles per workgroup in the scan passes
+constexpr int kScanTiles = 256;      // tiles per workgroup in the scan passes (one per thread)
+constexpr int kAtomicMaxSamples = 16384;  // problems this small take the atomic grad_value path
 
 // Everything one launch needs, passed by value as the kernel argument.
 struct Params {
@@ -73,6 +74,8 @@ hipError_t launch_backward_grads(const Params& p, msda_dtype_t dtype, bool atomi
 hipError_t launch_backward_value_binned(const Params& p, msda_dtype_t dtype, hipStream_t stream);
 hipError_t launch_zero(float* ptr, int64_t n, hipStream_t stream);
 
+// True when fp32 atomics are expected to beat the binned grad_value path (sparse or small problems).
+bool prefer_atomic(const Params& p);
 // Chooses tile sizes for the binned grad_value path and fills the geometry fields of `p`.
 // Returns false if the path does not apply (then grad_value uses atomics).
 bool plan_binned(Params& p);

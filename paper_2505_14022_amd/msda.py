@@ -22,6 +22,8 @@ MSDA_ERROR_LAUNCH_FAILED = 3
 MSDA_F32 = 0
 MSDA_F16 = 1
 MSDA_MAX_LEVELS = 16
+MSDA_WORKSPACE_PREFERRED = 0
+MSDA_WORKSPACE_OWNER = 1
 
 EXPORTED = ["msda_check_args", "msda_forward", "msda_backward", "msda_backward_workspace_size",
             "msda_status_string", "msda_last_error", "msda_version"]
@@ -51,7 +53,8 @@ def lib():
         L.msda_backward.argtypes = [vp, ip, ip, vp, vp, vp, vp, vp, vp, vp, ctypes.c_size_t] + [i64] * 7 + \
             [ctypes.c_int, vp]
         L.msda_backward.restype = ctypes.c_int
-        L.msda_backward_workspace_size.argtypes = [ip, ip] + [i64] * 7 + [ctypes.c_int, ctypes.POINTER(ctypes.c_size_t)]
+        L.msda_backward_workspace_size.argtypes = [ip, ip] + [i64] * 7 + [ctypes.c_int, ctypes.c_int,
+                                                                         ctypes.POINTER(ctypes.c_size_t)]
         L.msda_backward_workspace_size.restype = ctypes.c_int
         L.msda_status_string.argtypes = [ctypes.c_int]
         L.msda_status_string.restype = ctypes.c_char_p
@@ -132,11 +135,15 @@ def _dims(value, sampling_loc):
     return N, S, M, D, Lq, L, P
 
 
-def workspace_size(spatial_shapes, level_start_index, N, S, M, D, Lq, L, P, dtype) -> int:
-    """msda_backward_workspace_size: bytes of device workspace for the owner-computes grad_value."""
+def workspace_size(spatial_shapes, level_start_index, N, S, M, D, Lq, L, P, dtype,
+                   mode: int = MSDA_WORKSPACE_PREFERRED) -> int:
+    """msda_backward_workspace_size: bytes of device workspace for the owner-computes grad_value
+    (MSDA_WORKSPACE_PREFERRED: 0 where the library prefers atomics; MSDA_WORKSPACE_OWNER: the
+    owner-computes size wherever that path applies)."""
     sh, st = _host_tables(spatial_shapes, level_start_index)
     out = ctypes.c_size_t(0)
-    r = lib().msda_backward_workspace_size(_iptr(sh), _iptr(st), N, S, M, D, Lq, L, P, int(dtype), ctypes.byref(out))
+    r = lib().msda_backward_workspace_size(_iptr(sh), _iptr(st), N, S, M, D, Lq, L, P, int(dtype), int(mode),
+                                           ctypes.byref(out))
     _raise(r, "msda_backward_workspace_size")
     return int(out.value)
 
@@ -159,8 +166,9 @@ def backward(value, spatial_shapes, level_start_index, sampling_loc, attn_weight
              grad_value=None, grad_loc=None, grad_attn=None, workspace="auto", stream=None):
     """(grad_value fp32, grad_loc, grad_attn) from msda_backward.
 
-    workspace: "auto" allocates the size msda_backward_workspace_size reports (a uint8 device
-    tensor), None passes no workspace (grad_value by atomics), or a caller-owned uint8 tensor.
+    workspace: "auto" allocates the workspace the library prefers for this problem (none where
+    atomics are faster), "owner" the owner-computes workspace wherever that path applies, None
+    passes no workspace (grad_value by atomics); or a caller-owned uint8 device tensor.
     """
     import torch
 
@@ -173,8 +181,11 @@ def backward(value, spatial_shapes, level_start_index, sampling_loc, attn_weight
     if grad_attn is None:
         grad_attn = torch.empty(tuple(attn_weight.shape), dtype=torch.float32, device=dev)
     sh, st = _host_tables(spatial_shapes, level_start_index)
-    if isinstance(workspace, str) and workspace == "auto":
-        nbytes = workspace_size(sh.reshape(-1, 2), st, N, S, M, D, Lq, L, P, _dtype_code(value))
+    if isinstance(workspace, str):
+        if workspace not in ("auto", "owner"):
+            raise ValueError(f"workspace must be 'auto', 'owner', None or a tensor, not {workspace!r}")
+        mode = MSDA_WORKSPACE_PREFERRED if workspace == "auto" else MSDA_WORKSPACE_OWNER
+        nbytes = workspace_size(sh.reshape(-1, 2), st, N, S, M, D, Lq, L, P, _dtype_code(value), mode)
         workspace = torch.empty(max(nbytes, 1), dtype=torch.uint8, device=dev) if nbytes else None
     ws_ptr = _dptr(workspace) if workspace is not None else None
     ws_bytes = workspace.numel() * workspace.element_size() if workspace is not None else 0

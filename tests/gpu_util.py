@@ -60,7 +60,8 @@ def to_device(inp: workloads.Inputs) -> DeviceInputs:
 
 
 def run_gpu(inp: workloads.Inputs, backward: bool = True, workspace="auto"):
-    """Run libmsda on `inp`; workspace="auto" takes the owner-computes grad_value path, None the
+    """Run libmsda on `inp`; workspace="auto" takes the grad_value path the library prefers,
+    "owner" the owner-computes path wherever it applies, None the
     atomic one."""
     import torch
 

@@ -152,8 +152,9 @@ def test_backward_checks_pointers_before_launching(L):
                         0x5008, 0x6000, 0x7000, None, 0, *a[2:9], a[9], None)
     assert r == msda.MSDA_ERROR_INVALID_VALUE and "grad_value" in msda.last_error()
     # a workspace smaller than reported is rejected before anything is launched
+    a[6] = 2000  # enough samples for the owner-computes path to be preferred
     need = msda.workspace_size(a[0], a[1], *a[2:9], a[9])
-    assert need > 0
+    assert need > 0 and need == msda.workspace_size(a[0], a[1], *a[2:9], a[9], msda.MSDA_WORKSPACE_OWNER)
     r = L.msda_backward(0x1000, a[0].ctypes.data_as(ip), a[1].ctypes.data_as(ip), 0x2000, 0x3000, 0x4000,
                         0x5000, 0x6000, 0x7000, 0x8000, need - 1, *a[2:9], a[9], None)
     assert r == msda.MSDA_ERROR_INVALID_VALUE and "workspace" in msda.last_error()
@@ -164,16 +165,23 @@ def test_backward_checks_pointers_before_launching(L):
 
 @pytest.mark.parametrize("w", workloads.WORKLOADS, ids=lambda w: w.name)
 def test_workspace_sizes(L, w):
-    need = msda.workspace_size(*_args(w))
+    owner = msda.workspace_size(*_args(w), msda.MSDA_WORKSPACE_OWNER)
     # the owner-computes path applies to every workload; its scratch is one 16-byte record per
-    # sample plus a few counters per tile
-    assert 0 < need < 64 + 16 * w.samples + 64 * w.N * w.M * w.S, need
+    # sample plus a few integers per tile and per work item
+    assert 0 < owner < 64 + 16 * w.samples + 64 * w.N * w.M * w.S, owner
+    # the preferred size is 0 for problems with fewer than one sample per two value rows or at most
+    # 16384 samples (the DETR decoder and the tiny case), and the owner-computes size otherwise
+    sparse = 2 * w.samples < w.N * w.S * w.M or w.samples <= 16384
+    assert msda.workspace_size(*_args(w)) == (0 if sparse else owner)
 
 
 def test_workspace_size_not_applicable(L):
     a = base()
     a[5] = 3001  # D % 4 != 0 and D > 355: grad_value by atomics, no workspace
-    assert msda.workspace_size(a[0], a[1], *a[2:9], a[9]) == 0
+    assert msda.workspace_size(a[0], a[1], *a[2:9], a[9], msda.MSDA_WORKSPACE_OWNER) == 0
+    a = base()
+    with pytest.raises(msda.MsdaError):
+        msda.workspace_size(a[0], a[1], *a[2:9], a[9], 7)
     a = base()
     a[6] = 0  # nothing to do
     assert msda.workspace_size(a[0], a[1], *a[2:9], a[9]) == 0

@@ -42,13 +42,13 @@ SMALL = [
 ]
 
 
-@pytest.mark.parametrize("path", ["binned", "atomic"])
+@pytest.mark.parametrize("path", ["owner", "atomic"])
 @pytest.mark.parametrize("case", SMALL, ids=lambda c: f"N{c[0]}M{c[1]}D{c[2]}L{len(c[3])}P{c[4]}Lq{c[5]}{c[6]}")
 def test_small_parity(case, path):
     N, M, D, shapes, P, Lq, dt = case
     inp = workloads.random_case(N, M, D, shapes, P, Lq, dt, seed=1000 + D + Lq)
     say(f"small case {inp.w.name} ({path} grad_value)")
-    check_parity(inp, workspace="auto" if path == "binned" else None)
+    check_parity(inp, workspace="owner" if path == "owner" else None)
 
 
 @pytest.mark.parametrize("seed", range(3))
@@ -58,14 +58,14 @@ def test_dense_coarse_levels_split_tiles(seed):
     inp = workloads.random_case(2, 4, 32, ((12, 10), (3, 5), (1, 2)), 8, 3000, "f32", seed=40 + seed,
                                 lo=0.2, hi=0.6)
     say(f"split tiles seed {seed}")
-    check_parity(inp)
+    check_parity(inp, workspace="owner")
 
 
 @pytest.mark.parametrize("lo,hi", [(-0.6, 1.6), (0.0, 1.0), (0.45, 0.55)])
 def test_location_ranges(lo, hi):
     inp = workloads.random_case(2, 4, 32, ((13, 17), (7, 9)), 4, 123, "f32", seed=7, lo=lo, hi=hi)
     say(f"location range [{lo}, {hi}]")
-    check_parity(inp)
+    check_parity(inp, workspace="owner")
 
 
 @pytest.mark.parametrize("w", workloads.WORKLOADS, ids=lambda w: w.name)
@@ -73,6 +73,14 @@ def test_workload_full_size(w):
     say(f"full-size workload {w.name}: N={w.N} M={w.M} D={w.D} S={w.S} Lq={w.Lq} L={w.L} P={w.P} {w.dtype}")
     inp = workloads.generate(w)
     check_parity(inp)
+
+
+@pytest.mark.parametrize("name", ["tiny", "detr_decoder"])
+def test_sparse_workloads_owner_path(name):
+    # these take the atomic path by default; the owner-computes path must agree as well
+    w = workloads.BY_NAME[name]
+    say(f"full-size workload {w.name} with owner-computes grad_value")
+    check_parity(workloads.generate(w), workspace="owner")
 
 
 def test_workload_full_size_atomic_path():
