@@ -520,6 +520,8 @@ constexpr int kRunKeys = (kRunEdge + 1) << kKeyShift;
 constexpr int kKeysPerLane = (kRunKeys + 63) / 64;
 constexpr int kGroups = 8;                                 // lane groups per wave (8 lanes, 4 channels each)
 constexpr int kRunBatch = 16;                              // grad_out rows in flight per lane
+constexpr int kQueues = 8;                                 // fold work queues, one per XCD
+constexpr int kQueueStride = 64;                           // ints between queue counters (256 B)
 
 template <typename T, int VEC>
 struct QuadBuf;
@@ -607,18 +609,34 @@ __global__ __launch_bounds__(256, 2) void fold_runs_kernel(Params p) {
     const rsrc_t gr = make_rsrc(p.grad_out, (uint32_t)((size_t)p.n_batch * p.Lq * p.M * D * sizeof(T)));
     const int quad = lane & 7, grp = lane >> 3;
 
-    // Work items come from one queue in slab-major order, so the waves in flight at any time work
-    // on neighbouring tiles of a few slabs, spread over all XCDs. (Giving each XCD slabs of its
-    // own was slower: one head's rows lie 1 KB apart in the interleaved layouts, so an XCD working
-    // on a single head keeps few L2 channels busy.)
+    // Work items are dealt from eight queues: queue x holds items x, x + 8, x + 16, ... and serves
+    // the waves of XCD x (workgroups are dispatched to the eight XCDs in turn). The waves in flight
+    // still work on neighbouring items in slab-major order. Each counter has a 256-byte line of its
+    // own: all waves taking items from one counter (or from counters sharing a line) serialize on
+    // it, which cost the fold a quarter of its time. A wave whose queue has drained helps the others.
     const int total = p.tile_chunks[p.n_tiles];
+    int owner = blockIdx.x & (kQueues - 1), visited = 0;
+    auto owned = [&](int q) { return (total - q + kQueues - 1) / kQueues; };
+    auto counter = [&](int q) { return p.queue + q * kQueueStride; };
     int taken = 0;
-    if (lane == 0) taken = atomicAdd(p.queue, 1);
+    if (lane == 0) taken = atomicAdd(counter(owner), 1);
     for (;;) {
-        const int item = __builtin_amdgcn_readfirstlane(taken);
-        if (item >= total) break;
-        // the next item is taken now; it is needed only when this one is done
-        if (lane == 0) taken = atomicAdd(p.queue, 1);
+        const int slot = __builtin_amdgcn_readfirstlane(taken);
+        if (slot >= owned(owner)) {  // this queue has drained: go to the next one
+            if (++visited >= kQueues) break;
+            owner = (owner + 1) & (kQueues - 1);
+            int seen = 0;
+            if (lane == 0) seen = __hip_atomic_load(counter(owner), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            if (__builtin_amdgcn_readfirstlane(seen) >= owned(owner)) {
+                taken = owned(owner);  // drained already: no atomic needed
+            } else if (lane == 0) {
+                taken = atomicAdd(counter(owner), 1);
+            }
+            continue;
+        }
+        const int item = slot * kQueues + owner;
+        // the next slot is taken now; it is needed only when this item is done
+        if (lane == 0) taken = atomicAdd(counter(owner), 1);
         int dv = 0;
         if (lane < 16) dv = p.item_desc[(size_t)item * 16 + lane];
         const int beg = __builtin_amdgcn_readlane(dv, 0), end = __builtin_amdgcn_readlane(dv, 1);
@@ -922,7 +940,7 @@ int queue_grid() {
 
 size_t binned_workspace_bytes(const Params& p) {
     const size_t nb = (size_t)p.n_tiles * 4;
-    return align256((nb + 1) * 4) + align256((size_t)p.max_items * 64) + align256((nb + 1) * 4) + align256(nb * 4) +
+    return align256((nb + kQueues * kQueueStride) * 4) + align256((size_t)p.max_items * 64) + align256((nb + 1) * 4) + align256(nb * 4) +
            align256(((size_t)p.n_tiles + 1) * 4) +
            align256((size_t)p.max_items * 4) + align256((size_t)p.scan_blocks * 2 * 4) +
            align256((size_t)p.n_samples * 16);
@@ -933,7 +951,7 @@ void bind_workspace(Params& p, void* ws) {
     const size_t nb = (size_t)p.n_tiles * 4;
     p.counts = reinterpret_cast<int*>(c);
     p.queue = p.counts + nb;
-    c += align256((nb + 1) * 4);
+    c += align256((nb + kQueues * kQueueStride) * 4);
     p.item_desc = reinterpret_cast<int*>(c);
     c += align256((size_t)p.max_items * 64);
     p.offsets = reinterpret_cast<int*>(c);
@@ -951,7 +969,7 @@ void bind_workspace(Params& p, void* ws) {
 
 hipError_t launch_backward_value_binned(const Params& p0, msda_dtype_t dtype, hipStream_t stream) {
     Params p = p0;
-    hipError_t e = launch_zero(reinterpret_cast<float*>(p.counts), (int64_t)p.n_tiles * 4 + 1, stream);
+    hipError_t e = launch_zero(reinterpret_cast<float*>(p.counts), (int64_t)p.n_tiles * 4 + kQueues * kQueueStride, stream);
     if (e != hipSuccess) return e;
     p.q_per_block = kCountQueries / p.K > 0 ? kCountQueries / p.K : 1;
     p.chunks = (p.Lq + p.q_per_block - 1) / p.q_per_block;

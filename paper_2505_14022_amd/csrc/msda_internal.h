@@ -56,7 +56,7 @@ struct Params {
     int max_items;              // capacity of `items`
     int scan_blocks;            // ceil(n_tiles / kScanTiles)
     int* counts;                // [n_tiles * 4]       samples per (tile, class)
-    int* queue;                 // [1]                 next work item of the fold (zeroed with counts)
+    int* queue;                 // [8 * 64]            fold work queue counters, 256 B apart (zeroed with counts)
     int* item_desc;             // [max_items * 16]    fold work item descriptors
     int* offsets;               // [n_tiles * 4 + 1]   exclusive prefix of counts
     int* cursor;                // [n_tiles * 4]       fill position per bin
