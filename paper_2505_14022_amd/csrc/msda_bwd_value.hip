@@ -518,8 +518,15 @@ constexpr int kRunPix = kRunEdge * kRunEdge;
 constexpr int kKeyShift = 4;
 constexpr int kRunKeys = (kRunEdge + 1) << kKeyShift;
 constexpr int kKeysPerLane = (kRunKeys + 63) / 64;
-constexpr int kGroups = 8;                                 // lane groups per wave (8 lanes, 4 channels each)
-constexpr int kRunBatch = 16;                              // grad_out rows in flight per lane
+#ifndef MSDA_FOLD_LANES_PER_RECORD
+#define MSDA_FOLD_LANES_PER_RECORD 4
+#endif
+constexpr int kPixQ = 8;                          // float4 per 32-channel pixel row of the LDS tile
+constexpr int kLPR = MSDA_FOLD_LANES_PER_RECORD;  // lanes that share one record (32 channels)
+constexpr int kQPL = kPixQ / kLPR;                // float4 of a record's row per lane
+constexpr int kGroups = 64 / kLPR;                // record streams per wave
+constexpr int kRunBatch = 2 * kLPR;               // records in flight per stream (128 rows per wave)
+static_assert(kLPR == 2 || kLPR == 4 || kLPR == 8, "lanes per record");
 constexpr int kQueues = 8;                                 // fold work queues, one per XCD
 constexpr int kQueueStride = 64;                           // ints between queue counters (256 B)
 
@@ -552,32 +559,36 @@ __device__ __forceinline__ void add4(float4& a, float w, const float4& g) {
     a.w += w * g.w;
 }
 
+// Sums of one run for the lane's channels: corner k (00, 01, 10, 11), float4 j.
 struct Corners {
-    float4 v00, v01, v10, v11;
+    float4 v[4][kQPL];
 };
 
 // Adds the four corner sums of the run whose top-left corner has key `key` into the LDS tile
 // (pixels outside the tile belong to neighbouring tiles and are dropped). The corners are
-// written one after another, each read-add-write finished before the next begins: another lane
-// group may be adding the same pixel as a different corner of a different run.
-__device__ __forceinline__ void flush_run(float4* acc, int key, int TH, int TW, int quad, const Corners& c) {
+// written one after another, each read-add-write finished before the next begins: another record
+// stream may be adding the same pixel as a different corner of a different run.
+__device__ __forceinline__ void flush_run(float4* acc, int key, int TH, int TW, int sub, const Corners& c) {
     const int r = (key >> kKeyShift) - 1, col = (key & ((1 << kKeyShift) - 1)) - 1;
-    auto add_px = [&](int rr, int cc, const float4& v) {
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+        const int rr = r + (k >> 1), cc = col + (k & 1);
         if (rr >= 0 && rr < TH && cc >= 0 && cc < TW) {
-            float4* d = acc + (rr * TW + cc) * kGroups + quad;
-            float4 x = *d;
-            x.x += v.x;
-            x.y += v.y;
-            x.z += v.z;
-            x.w += v.w;
-            *d = x;
+            float4* d = acc + (rr * TW + cc) * kPixQ + sub * kQPL;
+            float4 x[kQPL];
+#pragma unroll
+            for (int j = 0; j < kQPL; ++j) x[j] = d[j];
+#pragma unroll
+            for (int j = 0; j < kQPL; ++j) {
+                x[j].x += c.v[k][j].x;
+                x[j].y += c.v[k][j].y;
+                x[j].z += c.v[k][j].z;
+                x[j].w += c.v[k][j].w;
+                d[j] = x[j];
+            }
         }
         __asm__ volatile("" ::: "memory");
-    };
-    add_px(r, col, c.v00);
-    add_px(r, col + 1, c.v01);
-    add_px(r + 1, col, c.v10);
-    add_px(r + 1, col + 1, c.v11);
+    }
 }
 
 // One wave per work item (a tile, or a chunk of a split tile's visible records), taken from a
@@ -585,12 +596,14 @@ __device__ __forceinline__ void flush_run(float4* acc, int key, int TH, int TW, 
 //   1. every lane loads kChunkRecords/64 records (all loads in flight together) and keys each by
 //      the tile position of its top-left corner; LDS counters rank the records per key;
 //   2. a scan over the keys gives each key's run start, and the records are placed in key order;
-//   3. the sorted records are cut into eight equal slices, one per group of eight lanes (four
-//      channels per lane). A group reads each record's grad_out row once and keeps the current
-//      run's four corner sums in registers; when the key changes the run is added into an LDS
-//      tile. A run that ends inside a slice ends in no other slice, so two groups never add the
-//      same key at once. The run a slice ends on may go on in the next slices: those last runs
-//      are added after the slices are done, one link of each chain of equal keys per round;
+//   3. the sorted records are cut into 64/kLPR equal slices, one per stream of kLPR lanes that
+//      share a record (32/kLPR channels per lane). A stream reads each record's grad_out row once
+//      and keeps the current run's four corner sums in registers; when the key changes the run is
+//      added into an LDS tile. A run that ends inside a slice ends in no other slice, so two
+//      streams never add the same key at once. The run a slice ends on may go on in the next
+//      slices: those last runs are added after the slices are done, one link of each chain of
+//      equal keys per round. (Fewer lanes per record spread the per-record work and the run ends
+//      over more streams: 4 lanes took 5 % off the backward against 8.)
 //   4. the tile's on-map pixels are stored once (plain stores), or added with atomics when the
 //      tile is split over several work items (its rows were zeroed before).
 // Every grad_out row read past a slice's end uses an out-of-range buffer offset, which returns zeros.
@@ -599,7 +612,7 @@ __global__ __launch_bounds__(256, 2) void fold_runs_kernel(Params p) {
     __shared__ int s_geo[kGeo * kMaxLevels];
     __shared__ int s_start[kAccWaves][kRunKeys + 1];
     __shared__ int4 s_rec[kAccWaves][kChunkRecords];        // records sorted by key
-    __shared__ float4 s_acc[kAccWaves][kRunPix * kGroups];  // 32 channels of the tile
+    __shared__ float4 s_acc[kAccWaves][kRunPix * kPixQ];    // 32 channels of the tile
     load_geo(p, s_geo);
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
     int* start = s_start[wave];
@@ -607,7 +620,7 @@ __global__ __launch_bounds__(256, 2) void fold_runs_kernel(Params p) {
     float4* acc = s_acc[wave];
     const int D = p.D;
     const rsrc_t gr = make_rsrc(p.grad_out, (uint32_t)((size_t)p.n_batch * p.Lq * p.M * D * sizeof(T)));
-    const int quad = lane & 7, grp = lane >> 3;
+    const int sub = lane % kLPR, grp = lane / kLPR;  // lane within its record stream, stream
 
     // Work items are dealt from eight queues: queue x holds items x, x + 8, x + 16, ... and serves
     // the waves of XCD x (workgroups are dispatched to the eight XCDs in turn). The waves in flight
@@ -739,10 +752,9 @@ __global__ __launch_bounds__(256, 2) void fold_runs_kernel(Params p) {
             const int4 e = srec[lo];
             key_lo = key_of(floorf(__builtin_bit_cast(float, e.z)), floorf(__builtin_bit_cast(float, e.w)));
         }
-        for (int ch0 = 0; ch0 < D; ch0 += 4 * kGroups) {
-            const int ch = ch0 + 4 * quad;
-            const bool ch_ok = ch < D;
-            for (int e = lane; e < kRunPix * kGroups; e += 64) acc[e] = make_float4(0.f, 0.f, 0.f, 0.f);
+        for (int ch0 = 0; ch0 < D; ch0 += 4 * kPixQ) {
+            const int ch = ch0 + 4 * kQPL * sub;  // the lane's first channel
+            for (int e = lane; e < kRunPix * kPixQ; e += 64) acc[e] = make_float4(0.f, 0.f, 0.f, 0.f);
             wave_lds_sync();
             int cur = key_lo;
             Corners run = {};
@@ -754,14 +766,17 @@ __global__ __launch_bounds__(256, 2) void fold_runs_kernel(Params p) {
                     const int pos = lo + b + u;
                     const bool act = pos < hi;
                     const int4 e = srec[act ? pos : 0];
-                    off[u] = act && ch_ok ? (uint32_t)(e.x + ch) : (uint32_t)kOOBElem;
+                    off[u] = act ? (uint32_t)(e.x + ch) : (uint32_t)kOOBElem;
                     ra[u] = act ? __builtin_bit_cast(float, e.y) : 0.f;
                     rh[u] = __builtin_bit_cast(float, e.z);
                     rw[u] = __builtin_bit_cast(float, e.w);
                 }
-                float4 g[kRunBatch];
+                float4 g[kRunBatch][kQPL];
 #pragma unroll
-                for (int u = 0; u < kRunBatch; ++u) g[u] = QuadBuf<T, 4>::load(gr, off[u]);
+                for (int u = 0; u < kRunBatch; ++u)
+#pragma unroll
+                    for (int j = 0; j < kQPL; ++j)  // channels past D read zeros (out-of-range offset)
+                        g[u][j] = QuadBuf<T, 4>::load(gr, ch + 4 * j < D ? off[u] + 4 * j : (uint32_t)kOOBElem);
 #pragma unroll
                 for (int u = 0; u < kRunBatch; ++u) {
                     const int pos = lo + b + u;
@@ -769,36 +784,37 @@ __global__ __launch_bounds__(256, 2) void fold_runs_kernel(Params p) {
                         const float h0f = floorf(rh[u]), w0f = floorf(rw[u]);
                         const int key = key_of(h0f, w0f);
                         if (key != cur) {  // the run of key `cur` ends before this record
-                            flush_run(acc, cur, TH, TW, quad, run);
+                            flush_run(acc, cur, TH, TW, sub, run);
                             run = Corners{};
                             cur = key;
                         }
                         const float lh = rh[u] - h0f, lw = rw[u] - w0f, hh = 1.f - lh, hw = 1.f - lw, a = ra[u];
-                        add4(run.v00, a * (hh * hw), g[u]);
-                        add4(run.v01, a * (hh * lw), g[u]);
-                        add4(run.v10, a * (lh * hw), g[u]);
-                        add4(run.v11, a * (lh * lw), g[u]);
+                        const float wk[4] = {a * (hh * hw), a * (hh * lw), a * (lh * hw), a * (lh * lw)};
+#pragma unroll
+                        for (int k = 0; k < 4; ++k)
+#pragma unroll
+                            for (int j = 0; j < kQPL; ++j) add4(run.v[k][j], wk[k], g[u][j]);
                     }
                 }
             }
             // the runs the slices end on: a key may end several neighbouring slices. Each slice
             // counts the earlier slices that end on its key; round j adds the sums of the slices
-            // with count j, so no two groups add the same key at once
+            // with count j, so no two streams add the same key at once
             const int last = hi > lo ? cur : -1;
             int link = 0;
 #pragma unroll
             for (int j = 0; j < kGroups; ++j) {
-                const int kj = __builtin_amdgcn_readlane(last, 8 * j);
+                const int kj = __builtin_amdgcn_readlane(last, kLPR * j);
                 link += (j < grp && kj == last) ? 1 : 0;
             }
 #pragma unroll 1
             for (int j = 0; j < kGroups; ++j)
-                if (last >= 0 && link == j) flush_run(acc, last, TH, TW, quad, run);
+                if (last >= 0 && link == j) flush_run(acc, last, TH, TW, sub, run);
             wave_lds_sync();
             // 4. store the tile's on-map pixels
             if (!split) {
-                for (int e = lane; e < kRunPix * kGroups; e += 64) {
-                    const int px = e / kGroups, q = e - px * kGroups;
+                for (int e = lane; e < kRunPix * kPixQ; e += 64) {
+                    const int px = e / kPixQ, q = e - px * kPixQ;
                     const int r = px >> tw, c = px & (TW - 1);
                     if (px < TH * TW && r < th_on && c < tw_on && ch0 + 4 * q < D) {
                         float* dst = p.grad_value + ((size_t)(n * p.S + st + (h_org + r) * W + w_org + c) * p.M + m) * D +
@@ -809,8 +825,8 @@ __global__ __launch_bounds__(256, 2) void fold_runs_kernel(Params p) {
             } else {
                 // one channel per lane: the atomics of a wave cover whole rows
                 const float* accf = reinterpret_cast<const float*>(acc);
-                for (int e = lane; e < kRunPix * 4 * kGroups; e += 64) {
-                    const int px = e / (4 * kGroups), cc = e - px * (4 * kGroups);
+                for (int e = lane; e < kRunPix * 4 * kPixQ; e += 64) {
+                    const int px = e / (4 * kPixQ), cc = e - px * (4 * kPixQ);
                     const int r = px >> tw, c = px & (TW - 1);
                     if (px < TH * TW && r < th_on && c < tw_on && ch0 + cc < D) {
                         float* dst = p.grad_value + ((size_t)(n * p.S + st + (h_org + r) * W + w_org + c) * p.M + m) * D +
