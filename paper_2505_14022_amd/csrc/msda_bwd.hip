@@ -33,6 +33,13 @@ __global__ __launch_bounds__(kBlock) void bwd_kernel(Params p) {
     const int q_mine = t.q0 + ps;
     const bool q_ok = q_mine < p.Lq;
     const size_t gout_row = ((size_t)(t.n * p.Lq + (q_ok ? q_mine : 0)) * p.M + t.m) * p.D;
+    // when the query's channels fit one pass of its lanes, its grad_out row is read once here
+    // instead of once per sample
+    const bool one_pass = p.D <= LPP * VEC;
+    float g_row[VEC];
+#pragma unroll
+    for (int i = 0; i < VEC; ++i) g_row[i] = 0.f;
+    if (one_pass && sub * VEC < p.D) Row<T, VEC>::load_ptr(g_row, gout + gout_row + sub * VEC);
 
     for (int k0 = 0; k0 < K; k0 += KC) {
         const int kn = K - k0 < KC ? K - k0 : KC;
@@ -58,7 +65,12 @@ __global__ __launch_bounds__(kBlock) void bwd_kernel(Params p) {
                 if (chan < p.D) {
                     const uint32_t cb = (uint32_t)chan << Row<T, VEC>::kShift;
                     float g[VEC], v0[VEC], v1[VEC], v2[VEC], v3[VEC];
-                    Row<T, VEC>::load_ptr(g, gout + gout_row + chan);
+                    if (one_pass) {
+#pragma unroll
+                        for (int i = 0; i < VEC; ++i) g[i] = g_row[i];
+                    } else {
+                        Row<T, VEC>::load_ptr(g, gout + gout_row + chan);
+                    }
                     Row<T, VEC>::load(v0, vr, ((uint32_t)off.x << Row<T, VEC>::kShift) + cb);
                     Row<T, VEC>::load(v1, vr, ((uint32_t)off.y << Row<T, VEC>::kShift) + cb);
                     Row<T, VEC>::load(v2, vr, ((uint32_t)off.z << Row<T, VEC>::kShift) + cb);
