@@ -45,6 +45,10 @@ def _load(path: str = _LIB_PATH):
     lib.msda_oracle_forward.restype = ctypes.c_int
     lib.msda_oracle_backward.argtypes = [dp, ip, ip, dp, dp, dp, dp, dp, dp] + [i64] * 7 + [ctypes.c_int, ctypes.c_int]
     lib.msda_oracle_backward.restype = ctypes.c_int
+    lib.msda_oracle_prologue.argtypes = [dp, dp, dp, ip] + [i64] * 5 + [ctypes.c_int, dp, dp]
+    lib.msda_oracle_prologue.restype = None
+    lib.msda_oracle_prologue_backward.argtypes = [dp, dp, dp, ip] + [i64] * 5 + [dp, dp, dp]
+    lib.msda_oracle_prologue_backward.restype = None
     return lib
 
 
@@ -119,3 +123,50 @@ def backward(value, shapes, starts, loc, attn, grad_out, coords_fp32: bool = Tru
                                    _ptr(ga, ctypes.c_double),
                                    N, S, M, D, Lq, L, P, int(bool(coords_fp32)), int(threads))
     return ((gv, gl, ga), used) if return_threads else (gv, gl, ga)
+
+
+def prologue(ref, offsets, logits, shapes, coords_fp32: bool = True, _lib_override=None):
+    """(loc [N,Lq,M,L,P,2], attn [N,Lq,M,L,P]) from reference points [N,Lq,L,2], offsets in pixels
+    [N,Lq,M,L,P,2] and attention logits [N,Lq,M,L*P] (float64)."""
+    ref, offsets, logits, shapes = _f64(ref), _f64(offsets), _f64(logits), _i64(shapes)
+    N, Lq, M, L, P, two = offsets.shape
+    assert two == 2 and ref.shape == (N, Lq, L, 2) and shapes.shape == (L, 2)
+    logits = logits.reshape(N, Lq, M, L * P)
+    loc = np.zeros(offsets.shape, dtype=np.float64)
+    attn = np.zeros(offsets.shape[:-1], dtype=np.float64)
+    L_ = _lib_override or lib()
+    L_.msda_oracle_prologue(_ptr(ref, ctypes.c_double), _ptr(offsets, ctypes.c_double),
+                            _ptr(logits, ctypes.c_double), _ptr(shapes, ctypes.c_int64), N, Lq, M, L, P,
+                            int(bool(coords_fp32)), _ptr(loc, ctypes.c_double), _ptr(attn, ctypes.c_double))
+    return loc, attn
+
+
+def prologue_backward(attn, grad_loc, grad_attn, shapes, _lib_override=None):
+    """(grad_offsets [N,Lq,M,L,P,2], grad_logits [N,Lq,M,L*P], grad_ref [N,Lq,L,2]) (float64)."""
+    attn, grad_loc, grad_attn, shapes = _f64(attn), _f64(grad_loc), _f64(grad_attn), _i64(shapes)
+    N, Lq, M, L, P, two = grad_loc.shape
+    g_off = np.zeros(grad_loc.shape, dtype=np.float64)
+    g_log = np.zeros((N, Lq, M, L * P), dtype=np.float64)
+    g_ref = np.zeros((N, Lq, L, 2), dtype=np.float64)
+    L_ = _lib_override or lib()
+    L_.msda_oracle_prologue_backward(_ptr(attn, ctypes.c_double), _ptr(grad_loc, ctypes.c_double),
+                                     _ptr(grad_attn, ctypes.c_double), _ptr(shapes, ctypes.c_int64),
+                                     N, Lq, M, L, P, _ptr(g_off, ctypes.c_double), _ptr(g_log, ctypes.c_double),
+                                     _ptr(g_ref, ctypes.c_double))
+    return g_off, g_log, g_ref
+
+
+def forward_fused(value, shapes, starts, ref, offsets, logits, coords_fp32: bool = True, threads: int = 0,
+                  _lib_override=None):
+    """out [N, Lq, M*D] of MSDA whose locations and weights come from the prologue."""
+    loc, attn = prologue(ref, offsets, logits, shapes, coords_fp32, _lib_override)
+    return forward(value, shapes, starts, loc, attn, coords_fp32, threads, _lib_override)
+
+
+def backward_fused(value, shapes, starts, ref, offsets, logits, grad_out, coords_fp32: bool = True,
+                   threads: int = 0, _lib_override=None):
+    """(grad_value, grad_offsets, grad_logits, grad_ref) of the fused operation (float64)."""
+    loc, attn = prologue(ref, offsets, logits, shapes, coords_fp32, _lib_override)
+    gv, gl, ga = backward(value, shapes, starts, loc, attn, grad_out, coords_fp32, threads, _lib_override)
+    g_off, g_log, g_ref = prologue_backward(attn, gl, ga, shapes, _lib_override)
+    return gv, g_off, g_log, g_ref

@@ -212,3 +212,90 @@ int msda_oracle_backward(const double* value, const int64_t* shapes, const int64
     }
     return used;
 }
+
+/*
+ * The step before the sampling (Sec. 4, first paragraph: the sampling coordinates and the
+ * attention weights are computed first, then the per-level bilinear sampling runs). A deformable
+ * attention layer predicts, for every sample, an offset in pixels of the sampled level and one
+ * attention logit. The location is the query's reference point on that level plus the offset
+ * divided by the level's size, and the weights of one (query, head) are a softmax over its L*P
+ * logits:
+ *   ref     [N, Lq, L, 2]       normalized (x, y) reference point per level
+ *   offsets [N, Lq, M, L, P, 2] pixels: x along W_l, y along H_l
+ *   logits  [N, Lq, M, L*P]
+ *   loc     [N, Lq, M, L, P, 2] = ref + offsets / (W_l, H_l)
+ *   attn    [N, Lq, M, L, P]    = softmax over the L*P logits of (n, q, m)
+ * With coords_fp32 the location is evaluated in fp32, the division and then the addition each
+ * rounded once, which is the arithmetic the GPU library uses, so both sample identical locations;
+ * otherwise in fp64 (finite-difference tests). The softmax is fp64, shifted by the maximum logit.
+ */
+void msda_oracle_prologue(const double* ref, const double* offsets, const double* logits,
+                          const int64_t* shapes, int64_t N, int64_t Lq, int64_t M, int64_t L, int64_t P,
+                          int coords_fp32, double* loc, double* attn)
+{
+    const int64_t K = L * P;
+#pragma omp parallel for schedule(static)
+    for (int64_t nq = 0; nq < N * Lq; ++nq) {
+        for (int64_t m = 0; m < M; ++m) {
+            const double* z = logits + (nq * M + m) * K;
+            double mx = z[0];
+            for (int64_t k = 1; k < K; ++k) mx = z[k] > mx ? z[k] : mx;
+            double sum = 0.0;
+            for (int64_t k = 0; k < K; ++k) sum += exp(z[k] - mx);
+            for (int64_t l = 0; l < L; ++l) {
+                const double W = (double)shapes[2 * l + 1], H = (double)shapes[2 * l];
+                const double rx = ref[(nq * L + l) * 2], ry = ref[(nq * L + l) * 2 + 1];
+                for (int64_t p = 0; p < P; ++p) {
+                    const int64_t k = l * P + p;
+                    const int64_t smp = (nq * M + m) * K + k;
+                    const double ox = offsets[2 * smp], oy = offsets[2 * smp + 1];
+                    if (coords_fp32) {
+                        const float fx = (float)ox / (float)W, fy = (float)oy / (float)H;
+                        loc[2 * smp] = (double)((float)rx + fx);
+                        loc[2 * smp + 1] = (double)((float)ry + fy);
+                    } else {
+                        loc[2 * smp] = rx + ox / W;
+                        loc[2 * smp + 1] = ry + oy / H;
+                    }
+                    attn[smp] = exp(z[k] - mx) / sum;
+                }
+            }
+        }
+    }
+}
+
+/*
+ * Gradients of the step above, from the sampling's grad_loc and grad_attn (chain rule):
+ *   grad_offsets = grad_loc / (W_l, H_l)
+ *   grad_logits  = attn * (grad_attn - sum_k attn_k grad_attn_k)   over the L*P samples of (n,q,m)
+ *   grad_ref     = sum over heads and points of grad_loc           [N, Lq, L, 2]
+ */
+void msda_oracle_prologue_backward(const double* attn, const double* grad_loc, const double* grad_attn,
+                                   const int64_t* shapes, int64_t N, int64_t Lq, int64_t M, int64_t L,
+                                   int64_t P, double* grad_offsets, double* grad_logits, double* grad_ref)
+{
+    const int64_t K = L * P;
+#pragma omp parallel for schedule(static)
+    for (int64_t nq = 0; nq < N * Lq; ++nq) {
+        for (int64_t l = 0; l < L; ++l) {
+            grad_ref[(nq * L + l) * 2] = 0.0;
+            grad_ref[(nq * L + l) * 2 + 1] = 0.0;
+        }
+        for (int64_t m = 0; m < M; ++m) {
+            const int64_t s0 = (nq * M + m) * K;
+            double dot = 0.0;
+            for (int64_t k = 0; k < K; ++k) dot += attn[s0 + k] * grad_attn[s0 + k];
+            for (int64_t l = 0; l < L; ++l) {
+                const double W = (double)shapes[2 * l + 1], H = (double)shapes[2 * l];
+                for (int64_t p = 0; p < P; ++p) {
+                    const int64_t smp = s0 + l * P + p;
+                    grad_offsets[2 * smp] = grad_loc[2 * smp] / W;
+                    grad_offsets[2 * smp + 1] = grad_loc[2 * smp + 1] / H;
+                    grad_logits[smp] = attn[smp] * (grad_attn[smp] - dot);
+                    grad_ref[(nq * L + l) * 2] += grad_loc[2 * smp];
+                    grad_ref[(nq * L + l) * 2 + 1] += grad_loc[2 * smp + 1];
+                }
+            }
+        }
+    }
+}

@@ -27,19 +27,23 @@ GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
 class Handle:
     forward: Callable
     backward: Callable
+    prologue: Callable = None
+    prologue_backward: Callable = None
 
 
 def real_handle() -> Handle:
     import oracle
 
-    return Handle(oracle.forward, oracle.backward)
+    return Handle(oracle.forward, oracle.backward, oracle.prologue, oracle.prologue_backward)
 
 
 def lib_handle(lib) -> Handle:
     import oracle
 
     return Handle(lambda *a, **k: oracle.forward(*a, _lib_override=lib, **k),
-                  lambda *a, **k: oracle.backward(*a, _lib_override=lib, **k))
+                  lambda *a, **k: oracle.backward(*a, _lib_override=lib, **k),
+                  lambda *a, **k: oracle.prologue(*a, _lib_override=lib, **k),
+                  lambda *a, **k: oracle.prologue_backward(*a, _lib_override=lib, **k))
 
 
 # ----------------------------------------------------------------------------- helpers
@@ -415,6 +419,125 @@ def pin_fp32_coordinates_are_rounding_only(h: Handle):
     close(a, b, 1e-5, "fp32 vs fp64 coordinates")
 
 
+# ----------------------------------------------------------------------------- prologue pins
+
+def pin_prologue_golden(h: Handle):
+    """Hand-derived prologue example (tests/golden/prologue_example.json), exact in binary."""
+    with open(os.path.join(GOLDEN, "prologue_example.json")) as f:
+        ex = json.load(f)
+    N, Lq, M, L, P = (ex[k] for k in ("N", "Lq", "M", "L", "P"))
+    shapes = np.asarray(ex["shapes"], dtype=np.int64)
+    ref = np.asarray(ex["ref"], dtype=np.float64).reshape(N, Lq, L, 2)
+    off = np.asarray(ex["offsets"], dtype=np.float64).reshape(N, Lq, M, L, P, 2)
+    logits = np.log(np.asarray(ex["logits_exp"], dtype=np.float64)).reshape(N, Lq, M, L * P)
+    loc, attn = h.prologue(ref, off, logits, shapes)
+    close(loc.reshape(-1, 2), ex["expected_loc"], 0.0, "prologue loc")
+    close(attn.reshape(-1), ex["expected_attn"], 1e-15, "prologue attn")
+    gl = np.asarray(ex["grad_loc"], dtype=np.float64).reshape(off.shape)
+    ga = np.asarray(ex["grad_attn"], dtype=np.float64).reshape(attn.shape)
+    g_off, g_log, g_ref = h.prologue_backward(np.asarray(ex["expected_attn"]).reshape(attn.shape), gl, ga, shapes)
+    close(g_off.reshape(-1, 2), ex["expected_grad_offsets"], 0.0, "prologue grad_offsets")
+    close(g_log.reshape(-1), ex["expected_grad_logits"], 1e-15, "prologue grad_logits")
+    close(g_ref.reshape(-1, 2), ex["expected_grad_ref"], 0.0, "prologue grad_ref")
+
+
+def _prologue_case(rng, N=2, Lq=5, M=3, shapes=((5, 7), (3, 4)), P=3):
+    shapes = np.asarray(shapes, dtype=np.int64).reshape(-1, 2)
+    L = shapes.shape[0]
+    ref = rng.uniform(0.1, 0.9, size=(N, Lq, L, 2)).astype(np.float32).astype(np.float64)
+    off = rng.normal(0.0, 2.0, size=(N, Lq, M, L, P, 2)).astype(np.float32).astype(np.float64)
+    logits = rng.normal(0.0, 1.0, size=(N, Lq, M, L * P)).astype(np.float32).astype(np.float64)
+    return shapes, ref, off, logits
+
+
+def pin_prologue_softmax_library(h: Handle):
+    """attn equals scipy's softmax over the L*P logits of each (query, head), is unchanged by
+    adding a constant to those logits, and sums to 1."""
+    from scipy.special import softmax
+
+    rng = np.random.default_rng(71)
+    shapes, ref, off, logits = _prologue_case(rng)
+    N, Lq, L = ref.shape[:3]
+    M, P = off.shape[2], off.shape[4]
+    _, attn = h.prologue(ref, off, logits, shapes)
+    close(attn.reshape(N, Lq, M, L * P), softmax(logits, axis=-1), 1e-14, "softmax vs scipy")
+    shift = rng.normal(0.0, 30.0, size=(N, Lq, M, 1))
+    _, attn2 = h.prologue(ref, off, logits + shift, shapes)
+    close(attn2, attn, 1e-13, "softmax shift invariance")
+    close(attn.reshape(N, Lq, M, -1).sum(-1), np.ones((N, Lq, M)), 1e-14, "softmax sums to 1")
+
+
+def pin_prologue_identity_cases(h: Handle):
+    """Zero offsets give the reference point itself (no rounding at all); equal logits give
+    weights 1/(L*P)."""
+    rng = np.random.default_rng(72)
+    shapes, ref, off, logits = _prologue_case(rng)
+    N, Lq, L = ref.shape[:3]
+    M, P = off.shape[2], off.shape[4]
+    loc, attn = h.prologue(ref, np.zeros_like(off), np.zeros_like(logits), shapes)
+    expect = np.broadcast_to(ref[:, :, None, :, None, :], loc.shape)
+    close(loc, expect, 0.0, "zero offsets")
+    close(attn, np.full(attn.shape, 1.0 / (L * P)), 1e-15, "equal logits")
+    # offsets of whole pixels move the location by whole pixels of the sampled level (fp64 mode)
+    k = rng.integers(-3, 4, size=off.shape).astype(np.float64)
+    loc2, _ = h.prologue(ref, k, logits, shapes, coords_fp32=False)
+    size = np.asarray([[w, hh] for hh, w in shapes], dtype=np.float64)  # (W_l, H_l)
+    moved = (loc2 - expect) * size[None, None, None, :, None, :]
+    close(moved, k, 1e-12, "offsets in pixels of the sampled level")
+
+
+def pin_prologue_finite_differences(h: Handle):
+    """Central differences of the fused forward (fp64 coordinates) w.r.t. offsets, logits and
+    reference points agree with the prologue backward chained after the sampling backward."""
+    rng = np.random.default_rng(73)
+    shapes, ref, off, logits = _prologue_case(rng, N=1, Lq=3, M=2)
+    N, Lq, L = ref.shape[:3]
+    M, P = off.shape[2], off.shape[4]
+    D = 3
+    S = int((shapes[:, 0] * shapes[:, 1]).sum())
+    starts = starts_of(shapes)
+    value = rng.standard_normal((N, S, M, D))
+    g = rng.standard_normal((N, Lq, M * D))
+
+    def f(ref_, off_, logits_):
+        loc, attn = h.prologue(ref_, off_, logits_, shapes, coords_fp32=False)
+        return float(np.sum(g * h.forward(value, shapes, starts, loc, attn, coords_fp32=False)))
+
+    loc, attn = h.prologue(ref, off, logits, shapes, coords_fp32=False)
+    _, gl, ga = h.backward(value, shapes, starts, loc, attn, g, coords_fp32=False)
+    g_off, g_log, g_ref = h.prologue_backward(attn, gl, ga, shapes)
+    eps = 1e-6
+    # distance of each sample's coordinates from a kink (integer h_im / w_im) or the range edge
+    size = np.asarray([[w, hh] for hh, w in shapes], dtype=np.float64)
+    im = loc * size[None, None, None, :, None, :] - 0.5
+    near = np.abs(im - np.round(im)) < 1e-3
+    safe = ~near.any(-1)
+    checked = 0
+    for idx in np.ndindex(*off.shape):
+        if not safe[idx[:-1]]:
+            continue
+        d = np.zeros_like(off)
+        d[idx] = eps
+        num = (f(ref, off + d, logits) - f(ref, off - d, logits)) / (2 * eps)
+        assert abs(num - g_off[idx]) <= 1e-6 * max(1.0, abs(num)), f"grad_offsets {idx}: fd {num} vs {g_off[idx]}"
+        checked += 1
+    for idx in np.ndindex(*logits.shape):
+        d = np.zeros_like(logits)
+        d[idx] = eps
+        num = (f(ref, off, logits + d) - f(ref, off, logits - d)) / (2 * eps)
+        assert abs(num - g_log[idx]) <= 1e-6 * max(1.0, abs(num)), f"grad_logits {idx}: fd {num} vs {g_log[idx]}"
+    # reference points move every sample of their level: skip levels with a sample near a kink
+    for idx in np.ndindex(*ref.shape):
+        n, q, l, c = idx
+        if not safe[n, q, :, l, :].all():
+            continue
+        d = np.zeros_like(ref)
+        d[idx] = eps
+        num = (f(ref + d, off, logits) - f(ref - d, off, logits)) / (2 * eps)
+        assert abs(num - g_ref[idx]) <= 1e-6 * max(1.0, abs(num)), f"grad_ref {idx}: fd {num} vs {g_ref[idx]}"
+    assert checked > off.size // 2, f"too few samples away from kinks ({checked})"
+
+
 ALL_PINS = [
     pin_golden_hand_example,
     pin_pixel_centres_gather,
@@ -428,6 +551,10 @@ ALL_PINS = [
     pin_level_decomposition,
     pin_head_batch_permutation,
     pin_fp32_coordinates_are_rounding_only,
+    pin_prologue_golden,
+    pin_prologue_softmax_library,
+    pin_prologue_identity_cases,
+    pin_prologue_finite_differences,
 ]
 
 

@@ -50,6 +50,17 @@ MUTANTS = {
     "grad_value_level_start_dropped": ("double* gv = grad_value + ((n * S + starts[l] + c.pix[k]) * M + m) * D;",
                                        "double* gv = grad_value + ((n * S + c.pix[k]) * M + m) * D;"),
     "grad_value_wrong_corner": ("gv[d] += a * c.wt[k] * g[d];", "gv[d] += a * c.wt[3 - k] * g[d];"),
+    "prologue_x_offset_scaled_by_H": ("(float)ox / (float)W", "(float)ox / (float)H"),
+    "prologue_y_offset_not_normalized": ("fy = (float)oy / (float)H", "fy = (float)oy"),
+    "prologue_fp64_offset_dropped": ("loc[2 * smp] = rx + ox / W;", "loc[2 * smp] = rx;"),
+    "prologue_softmax_unnormalized": ("attn[smp] = exp(z[k] - mx) / sum;", "attn[smp] = exp(z[k] - mx);"),
+    "prologue_softmax_wrong_row": ("const double* z = logits + (nq * M + m) * K;", "const double* z = logits + nq * K;"),
+    "prologue_grad_logits_no_dot": ("grad_logits[smp] = attn[smp] * (grad_attn[smp] - dot);",
+                                    "grad_logits[smp] = attn[smp] * grad_attn[smp];"),
+    "prologue_grad_offsets_times_W": ("grad_offsets[2 * smp] = grad_loc[2 * smp] / W;",
+                                      "grad_offsets[2 * smp] = grad_loc[2 * smp] * W;"),
+    "prologue_grad_ref_y_dropped": ("grad_ref[(nq * L + l) * 2 + 1] += grad_loc[2 * smp + 1];",
+                                    "grad_ref[(nq * L + l) * 2 + 1] += 0.0;"),
 }
 
 
