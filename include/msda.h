@@ -131,6 +131,72 @@ msda_status_t msda_backward_workspace_size(const int64_t* spatial_shapes, const 
                                            int64_t N, int64_t S, int64_t M, int64_t D, int64_t Lq,
                                            int64_t L, int64_t P, int dtype, int mode, size_t* bytes);
 
+/*
+ * Fused entry points: the step before the sampling (Sec. 4, first paragraph: the sampling
+ * coordinates and the attention weights are computed first) is done inside the library, from the
+ * layer's predictions, instead of being passed in as sampling_loc / attn_weight:
+ *
+ *   ref_points [N, Lq, L, 2]        fp32, (x, y) normalized reference point of each query per level
+ *   offsets    [N, Lq, M, L, P, 2]  fp32, (dx, dy) sampling offsets in PIXELS of level l
+ *   logits     [N, Lq, M, L*P]      fp32, attention logits; the weights are their softmax over
+ *                                   the L*P samples of one (query, head)
+ *
+ *   sampling_loc[n,q,m,l,p] = ref_points[n,q,l] + offsets[n,q,m,l,p] / (W_l, H_l)
+ *                             (fp32: the division and then the addition, each rounded once)
+ *   attn_weight[n,q,m,:]    = softmax(logits[n,q,m,:])
+ *
+ * after which the operation is the one of msda_forward / msda_backward.
+ */
+
+/*
+ * Fused forward: out = MSDA(value, sampling_loc(ref_points, offsets), softmax(logits)); the
+ * locations and weights are formed in registers and never stored. value and out 16-byte aligned;
+ * ref_points and offsets 8-byte; logits 4-byte. N*Lq == 0 is a successful no-op.
+ */
+msda_status_t msda_forward_fused(const void* value, const int64_t* spatial_shapes,
+                                 const int64_t* level_start_index, const float* ref_points,
+                                 const float* offsets, const float* logits, void* out,
+                                 int64_t N, int64_t S, int64_t M, int64_t D, int64_t Lq, int64_t L,
+                                 int64_t P, int dtype, void* stream);
+
+/*
+ * Workspace bytes for msda_backward_fused (host-only; modes and checks as for
+ * msda_backward_workspace_size). It is the staging of sampling_loc, attn_weight and their
+ * gradients for one launch's batch items (24 bytes per sample, 0 for an empty problem) plus
+ * msda_backward_workspace_size(..., mode, ...).
+ */
+msda_status_t msda_backward_fused_workspace_size(const int64_t* spatial_shapes,
+                                                 const int64_t* level_start_index, int64_t N,
+                                                 int64_t S, int64_t M, int64_t D, int64_t Lq,
+                                                 int64_t L, int64_t P, int dtype, int mode,
+                                                 size_t* bytes);
+
+/*
+ * Fused backward: given grad_out, write grad_value (as msda_backward) and the gradients of the
+ * predictions:
+ *   grad_offsets [N, Lq, M, L, P, 2] fp32 = grad_loc / (W_l, H_l)
+ *   grad_logits  [N, Lq, M, L*P]     fp32 = attn * (grad_attn - sum over the L*P samples of
+ *                                           attn * grad_attn)            (softmax chain rule)
+ *   grad_ref     [N, Lq, L, 2]       fp32 = sum over heads and points of grad_loc; may be NULL
+ *                                           (not computed)
+ * where grad_loc / grad_attn are msda_backward's outputs for the derived sampling_loc / weights.
+ *
+ * workspace is required whenever N*Lq > 0: at least the staging part of
+ * msda_backward_fused_workspace_size, 256-byte aligned, owned by the caller and not used by
+ * anything else until the enqueued work completes. grad_value is computed owner-by-owner when the
+ * workspace also holds msda_backward_workspace_size(..., MSDA_WORKSPACE_OWNER, ...) more bytes,
+ * else with fp32 atomics. A smaller workspace, or a null one, is an error.
+ * value and grad_out 16-byte aligned; grad_value 16-byte; ref_points, offsets, grad_offsets and
+ * grad_ref 8-byte; logits and grad_logits 4-byte. N*Lq == 0 still zeroes grad_value.
+ */
+msda_status_t msda_backward_fused(const void* value, const int64_t* spatial_shapes,
+                                  const int64_t* level_start_index, const float* ref_points,
+                                  const float* offsets, const float* logits, const void* grad_out,
+                                  float* grad_value, float* grad_ref, float* grad_offsets,
+                                  float* grad_logits, void* workspace, size_t workspace_bytes,
+                                  int64_t N, int64_t S, int64_t M, int64_t D, int64_t Lq, int64_t L,
+                                  int64_t P, int dtype, void* stream);
+
 /* Static name of a status code ("MSDA_SUCCESS", ...). */
 const char* msda_status_string(msda_status_t status);
 

@@ -96,6 +96,107 @@ msda::Params base_params(const int64_t* shapes, const int64_t* starts, int64_t S
     return p;
 }
 
+size_t round_up(int64_t b) { return (size_t)((b + 255) / 256 * 256); }
+
+// Sampling locations / weights and their gradients, per batch chunk: the caller's arrays (plain
+// entry points) or staging buffers of one chunk (fused entry points; `ref`.. of Prologue are set).
+struct Sampling {
+    const float* loc;
+    const float* attn;
+    float* grad_loc;
+    float* grad_attn;
+};
+
+// The fused entry points' inputs and outputs: the layer's predictions and their gradients.
+struct Prologue {
+    const float* ref;
+    const float* offsets;
+    const float* logits;
+    float* grad_ref;
+    float* grad_offsets;
+    float* grad_logits;
+};
+
+int64_t fused_batch_per_call(int64_t N, int64_t S, int64_t M, int64_t D, int64_t Lq, int64_t L, int64_t P) {
+    const int64_t nb = batch_per_launch(S, M, D, Lq, L, P);
+    return N < nb ? N : nb;
+}
+
+// Bytes of the fused backward's staging: loc, attn, grad_loc, grad_attn of one batch chunk.
+size_t fused_staging_bytes(int64_t N, int64_t S, int64_t M, int64_t D, int64_t Lq, int64_t L, int64_t P) {
+    const int64_t per = fused_batch_per_call(N, S, M, D, Lq, L, P) * Lq * M * L * P;
+    return 2 * round_up(per * 8) + 2 * round_up(per * 4);
+}
+
+// Shared body of both backward entry points (arguments already checked, except value / grad_out /
+// grad_value). `pro` is null for the plain entry point; with it, each batch chunk first computes
+// its locations and weights into the staging buffers of `smp` and ends with the prologue's gradient.
+// `workspace` non-null selects the binned grad_value.
+msda_status_t backward_body(const void* value, const int64_t* shapes, const int64_t* starts, const void* grad_out,
+                            float* grad_value, const Sampling& smp, const Prologue* pro, void* workspace, int64_t N,
+                            int64_t S, int64_t M, int64_t D, int64_t Lq, int64_t L, int64_t P, int dtype,
+                            hipStream_t s) {
+    if (!grad_value) return fail(MSDA_ERROR_INVALID_VALUE, "grad_value must be non-null");
+    if (!aligned(grad_value, 16)) return fail(MSDA_ERROR_INVALID_VALUE, "misaligned grad_value: 16 bytes needed");
+    if (Lq == 0) {
+        hipError_t e = msda::launch_zero(grad_value, N * S * M * D, s);
+        if (e != hipSuccess) return fail(MSDA_ERROR_LAUNCH_FAILED, "grad_value zeroing: %s", hipGetErrorString(e));
+        return ok();
+    }
+    if (!value || !grad_out) return fail(MSDA_ERROR_INVALID_VALUE, "value and grad_out must be non-null");
+    if (!aligned(value, 16) || !aligned(grad_out, 16))
+        return fail(MSDA_ERROR_INVALID_VALUE, "misaligned pointer: value and grad_out need 16 bytes");
+    const bool binned = workspace != nullptr;
+    const int es = elem_size(dtype);
+    const int64_t nb = batch_per_launch(S, M, D, Lq, L, P);
+    if (!binned) {
+        hipError_t e = msda::launch_zero(grad_value, N * S * M * D, s);
+        if (e != hipSuccess) return fail(MSDA_ERROR_LAUNCH_FAILED, "grad_value zeroing: %s", hipGetErrorString(e));
+    }
+    for (int64_t n0 = 0; n0 < N; n0 += nb) {
+        const int64_t cnt = N - n0 < nb ? N - n0 : nb;
+        const int64_t smp0 = pro ? 0 : n0 * Lq * M * L * P;  // staging holds one chunk
+        msda::Params p = base_params(shapes, starts, S, M, D, Lq, L, P);
+        p.n_batch = (int)cnt;
+        p.value = static_cast<const char*>(value) + n0 * S * M * D * es;
+        p.loc = smp.loc + smp0 * 2;
+        p.attn = smp.attn + smp0;
+        p.grad_out = static_cast<const char*>(grad_out) + n0 * Lq * M * D * es;
+        p.grad_value = grad_value + n0 * S * M * D;
+        p.grad_loc = smp.grad_loc + smp0 * 2;
+        p.grad_attn = smp.grad_attn + smp0;
+        p.value_bytes = (uint32_t)(cnt * S * M * D * es);
+        p.gv_bytes = (uint32_t)(cnt * S * M * D * 4);
+        hipError_t e = hipSuccess;
+        if (pro) {
+            p.ref = pro->ref + n0 * Lq * L * 2;
+            p.pix_offsets = pro->offsets + n0 * Lq * M * L * P * 2;
+            p.logits = pro->logits + n0 * Lq * M * L * P;
+            e = msda::launch_prologue(p, const_cast<float*>(p.loc), const_cast<float*>(p.attn), s);
+            if (e != hipSuccess) return fail(MSDA_ERROR_LAUNCH_FAILED, "prologue launch: %s", hipGetErrorString(e));
+        }
+        e = msda::launch_backward_grads(p, (msda_dtype_t)dtype, !binned, s);
+        if (e != hipSuccess) return fail(MSDA_ERROR_LAUNCH_FAILED, "backward launch: %s", hipGetErrorString(e));
+        if (binned) {
+            if (!msda::plan_binned(p))
+                return fail(MSDA_ERROR_LAUNCH_FAILED, "internal: binned plan changed between batches");
+            msda::bind_workspace(p, workspace);
+            e = msda::launch_backward_value_binned(p, (msda_dtype_t)dtype, s);
+            if (e != hipSuccess)
+                return fail(MSDA_ERROR_LAUNCH_FAILED, "backward grad_value launch: %s", hipGetErrorString(e));
+        }
+        if (pro) {
+            const int64_t q0 = n0 * Lq * M * L * P;
+            e = msda::launch_prologue_grad(p, p.attn, p.grad_loc, p.grad_attn, pro->grad_offsets + q0 * 2,
+                                           pro->grad_logits + q0,
+                                           pro->grad_ref ? pro->grad_ref + n0 * Lq * L * 2 : nullptr, s);
+            if (e != hipSuccess)
+                return fail(MSDA_ERROR_LAUNCH_FAILED, "prologue gradient launch: %s", hipGetErrorString(e));
+        }
+    }
+    return ok();
+}
+
 }  // namespace
 
 extern "C" {
@@ -160,27 +261,17 @@ msda_status_t msda_backward(const void* value, const int64_t* spatial_shapes, co
     msda_status_t st = check_problem(spatial_shapes, level_start_index, N, S, M, D, Lq, L, P, dtype);
     if (st != MSDA_SUCCESS) return st;
     if (N == 0) return ok();
-    if (!grad_value) return fail(MSDA_ERROR_INVALID_VALUE, "grad_value must be non-null");
-    if (!aligned(grad_value, 16)) return fail(MSDA_ERROR_INVALID_VALUE, "misaligned grad_value: 16 bytes needed");
-    hipStream_t s = (hipStream_t)stream;
-    if (Lq == 0) {
-        hipError_t e = msda::launch_zero(grad_value, N * S * M * D, s);
-        if (e != hipSuccess) return fail(MSDA_ERROR_LAUNCH_FAILED, "grad_value zeroing: %s", hipGetErrorString(e));
-        return ok();
+    if (Lq > 0) {
+        if (!sampling_loc || !attn_weight || !grad_loc || !grad_attn)
+            return fail(MSDA_ERROR_INVALID_VALUE,
+                        "value, sampling_loc, attn_weight, grad_out, grad_loc and grad_attn must be non-null");
+        if (!aligned(sampling_loc, 8) || !aligned(grad_loc, 8) || !aligned(attn_weight, 4) || !aligned(grad_attn, 4))
+            return fail(MSDA_ERROR_INVALID_VALUE,
+                        "misaligned pointer: value and grad_out need 16 bytes, sampling_loc and grad_loc 8, "
+                        "attn_weight and grad_attn 4");
     }
-    if (!value || !sampling_loc || !attn_weight || !grad_out || !grad_loc || !grad_attn)
-        return fail(MSDA_ERROR_INVALID_VALUE,
-                    "value, sampling_loc, attn_weight, grad_out, grad_loc and grad_attn must be non-null");
-    if (!aligned(value, 16) || !aligned(grad_out, 16) || !aligned(sampling_loc, 8) || !aligned(grad_loc, 8) ||
-        !aligned(attn_weight, 4) || !aligned(grad_attn, 4))
-        return fail(MSDA_ERROR_INVALID_VALUE,
-                    "misaligned pointer: value and grad_out need 16 bytes, sampling_loc and grad_loc 8, "
-                    "attn_weight and grad_attn 4");
-    const int es = elem_size(dtype);
-    const int64_t nb = batch_per_launch(S, M, D, Lq, L, P);
-    // binned (owner-computes) grad_value when a workspace is given and the problem fits it
     bool binned = false;
-    if (workspace) {
+    if (workspace && Lq > 0) {
         size_t need = 0;
         msda_backward_workspace_size(spatial_shapes, level_start_index, N, S, M, D, Lq, L, P, dtype,
                                      MSDA_WORKSPACE_OWNER, &need);
@@ -192,35 +283,98 @@ msda_status_t msda_backward(const void* value, const int64_t* spatial_shapes, co
             binned = true;
         }
     }
-    if (!binned) {
-        hipError_t e = msda::launch_zero(grad_value, N * S * M * D, s);
-        if (e != hipSuccess) return fail(MSDA_ERROR_LAUNCH_FAILED, "grad_value zeroing: %s", hipGetErrorString(e));
-    }
+    Sampling smp = {sampling_loc, attn_weight, grad_loc, grad_attn};
+    return backward_body(value, spatial_shapes, level_start_index, grad_out, grad_value, smp, nullptr,
+                         binned ? workspace : nullptr, N, S, M, D, Lq, L, P, dtype, (hipStream_t)stream);
+}
+
+msda_status_t msda_forward_fused(const void* value, const int64_t* spatial_shapes, const int64_t* level_start_index,
+                                 const float* ref_points, const float* offsets, const float* logits, void* out,
+                                 int64_t N, int64_t S, int64_t M, int64_t D, int64_t Lq, int64_t L, int64_t P,
+                                 int dtype, void* stream) {
+    msda_status_t st = check_problem(spatial_shapes, level_start_index, N, S, M, D, Lq, L, P, dtype);
+    if (st != MSDA_SUCCESS) return st;
+    if (N * Lq == 0) return ok();
+    if (!value || !ref_points || !offsets || !logits || !out)
+        return fail(MSDA_ERROR_INVALID_VALUE, "value, ref_points, offsets, logits and out must be non-null");
+    if (!aligned(value, 16) || !aligned(out, 16) || !aligned(ref_points, 8) || !aligned(offsets, 8) ||
+        !aligned(logits, 4))
+        return fail(MSDA_ERROR_INVALID_VALUE,
+                    "misaligned pointer: value and out need 16 bytes, ref_points and offsets 8, logits 4");
+    const int es = elem_size(dtype);
+    const int64_t nb = batch_per_launch(S, M, D, Lq, L, P);
     for (int64_t n0 = 0; n0 < N; n0 += nb) {
         const int64_t cnt = N - n0 < nb ? N - n0 : nb;
         msda::Params p = base_params(spatial_shapes, level_start_index, S, M, D, Lq, L, P);
         p.n_batch = (int)cnt;
         p.value = static_cast<const char*>(value) + n0 * S * M * D * es;
-        p.loc = sampling_loc + n0 * Lq * M * L * P * 2;
-        p.attn = attn_weight + n0 * Lq * M * L * P;
-        p.grad_out = static_cast<const char*>(grad_out) + n0 * Lq * M * D * es;
-        p.grad_value = grad_value + n0 * S * M * D;
-        p.grad_loc = grad_loc + n0 * Lq * M * L * P * 2;
-        p.grad_attn = grad_attn + n0 * Lq * M * L * P;
+        p.ref = ref_points + n0 * Lq * L * 2;
+        p.pix_offsets = offsets + n0 * Lq * M * L * P * 2;
+        p.logits = logits + n0 * Lq * M * L * P;
+        p.out = static_cast<char*>(out) + n0 * Lq * M * D * es;
         p.value_bytes = (uint32_t)(cnt * S * M * D * es);
-        p.gv_bytes = (uint32_t)(cnt * S * M * D * 4);
-        hipError_t e = msda::launch_backward_grads(p, (msda_dtype_t)dtype, !binned, s);
-        if (e != hipSuccess) return fail(MSDA_ERROR_LAUNCH_FAILED, "backward launch: %s", hipGetErrorString(e));
-        if (binned) {
-            if (!msda::plan_binned(p))
-                return fail(MSDA_ERROR_LAUNCH_FAILED, "internal: binned plan changed between batches");
-            msda::bind_workspace(p, workspace);
-            e = msda::launch_backward_value_binned(p, (msda_dtype_t)dtype, s);
-            if (e != hipSuccess)
-                return fail(MSDA_ERROR_LAUNCH_FAILED, "backward grad_value launch: %s", hipGetErrorString(e));
-        }
+        hipError_t e = msda::launch_forward_fused(p, (msda_dtype_t)dtype, (hipStream_t)stream);
+        if (e != hipSuccess) return fail(MSDA_ERROR_LAUNCH_FAILED, "fused forward launch: %s", hipGetErrorString(e));
     }
     return ok();
+}
+
+msda_status_t msda_backward_fused_workspace_size(const int64_t* spatial_shapes, const int64_t* level_start_index,
+                                                 int64_t N, int64_t S, int64_t M, int64_t D, int64_t Lq, int64_t L,
+                                                 int64_t P, int dtype, int mode, size_t* bytes) {
+    if (!bytes) return fail(MSDA_ERROR_INVALID_VALUE, "bytes must be non-null");
+    *bytes = 0;
+    size_t binned = 0;
+    msda_status_t st = msda_backward_workspace_size(spatial_shapes, level_start_index, N, S, M, D, Lq, L, P, dtype,
+                                                    mode, &binned);
+    if (st != MSDA_SUCCESS) return st;
+    if (N * Lq == 0) return ok();
+    *bytes = fused_staging_bytes(N, S, M, D, Lq, L, P) + binned;
+    return ok();
+}
+
+msda_status_t msda_backward_fused(const void* value, const int64_t* spatial_shapes,
+                                  const int64_t* level_start_index, const float* ref_points, const float* offsets,
+                                  const float* logits, const void* grad_out, float* grad_value, float* grad_ref,
+                                  float* grad_offsets, float* grad_logits, void* workspace, size_t workspace_bytes,
+                                  int64_t N, int64_t S, int64_t M, int64_t D, int64_t Lq, int64_t L, int64_t P,
+                                  int dtype, void* stream) {
+    msda_status_t st = check_problem(spatial_shapes, level_start_index, N, S, M, D, Lq, L, P, dtype);
+    if (st != MSDA_SUCCESS) return st;
+    if (N == 0) return ok();
+    size_t staging = 0, binned_need = 0;
+    if (Lq > 0) {
+        if (!ref_points || !offsets || !logits || !grad_offsets || !grad_logits)
+            return fail(MSDA_ERROR_INVALID_VALUE,
+                        "value, ref_points, offsets, logits, grad_out, grad_offsets and grad_logits must be non-null");
+        if (!aligned(ref_points, 8) || !aligned(offsets, 8) || !aligned(grad_offsets, 8) || !aligned(logits, 4) ||
+            !aligned(grad_logits, 4) || (grad_ref && !aligned(grad_ref, 8)))
+            return fail(MSDA_ERROR_INVALID_VALUE,
+                        "misaligned pointer: value and grad_out need 16 bytes, ref_points, offsets, grad_offsets "
+                        "and grad_ref 8, logits and grad_logits 4");
+        staging = fused_staging_bytes(N, S, M, D, Lq, L, P);
+        if (!workspace || workspace_bytes < staging)
+            return fail(MSDA_ERROR_INVALID_VALUE, "workspace of %zu bytes is smaller than the %zu needed",
+                        workspace ? workspace_bytes : (size_t)0, staging);
+        if (!aligned(workspace, 256)) return fail(MSDA_ERROR_INVALID_VALUE, "workspace must be 256-byte aligned");
+        msda_backward_workspace_size(spatial_shapes, level_start_index, N, S, M, D, Lq, L, P, dtype,
+                                     MSDA_WORKSPACE_OWNER, &binned_need);
+    }
+    // binned grad_value when the workspace also holds the binning buffers
+    const bool binned = binned_need > 0 && workspace_bytes >= staging + binned_need;
+    const int64_t nbmax = fused_batch_per_call(N, S, M, D, Lq, L, P);
+    const int64_t per = nbmax * Lq * M * L * P;  // samples staged per batch chunk
+    char* ws = static_cast<char*>(workspace);
+    Sampling smp = {};
+    if (Lq > 0) {
+        smp.loc = reinterpret_cast<float*>(ws);
+        smp.attn = reinterpret_cast<float*>(ws + round_up(per * 8));
+        smp.grad_loc = reinterpret_cast<float*>(ws + round_up(per * 8) + round_up(per * 4));
+        smp.grad_attn = reinterpret_cast<float*>(ws + 2 * round_up(per * 8) + round_up(per * 4));
+    }
+    Prologue pro = {ref_points, offsets, logits, grad_ref, grad_offsets, grad_logits};
+    return backward_body(value, spatial_shapes, level_start_index, grad_out, grad_value, smp, &pro,
+                         binned ? ws + staging : nullptr, N, S, M, D, Lq, L, P, dtype, (hipStream_t)stream);
 }
 
 const char* msda_status_string(msda_status_t status) {

@@ -147,6 +147,17 @@ __device__ __forceinline__ float dpp(float v) {
 // Steps 1-2 swap within quads (quad_perm), step 3 mirrors within 8 lanes (each lane meets the
 // other quad), step 4 mirrors within 16 lanes (each lane meets the other 8), then bpermute.
 template <int LPP>
+__device__ __forceinline__ float group_max(float v) {
+    if constexpr (LPP >= 2) v = fmaxf(v, dpp<0xB1>(v));
+    if constexpr (LPP >= 4) v = fmaxf(v, dpp<0x4E>(v));
+    if constexpr (LPP >= 8) v = fmaxf(v, dpp<0x141>(v));
+    if constexpr (LPP >= 16) v = fmaxf(v, dpp<0x140>(v));
+    if constexpr (LPP >= 32) v = fmaxf(v, __shfl_xor(v, 16, 64));
+    if constexpr (LPP >= 64) v = fmaxf(v, __shfl_xor(v, 32, 64));
+    return v;
+}
+
+template <int LPP>
 __device__ __forceinline__ float group_sum(float v) {
     if constexpr (LPP >= 2) v += dpp<0xB1>(v);   // quad_perm [1,0,3,2]
     if constexpr (LPP >= 4) v += dpp<0x4E>(v);   // quad_perm [2,3,0,1]
@@ -185,21 +196,18 @@ struct SampleDesc {
     float a, lh, lw;
 };
 
-// Coordinates, range test, floor and corner rows of one sample (Sec. 3: the 2x2 neighbourhood).
-// h_im / w_im are formed with one fp32 rounding, so floor() decisions are reproducible.
-__device__ __forceinline__ void describe(const Params& p, const int* s_lvl, int n, int m, int q, int k,
-                                         bool fold_attn, SampleDesc& sd) {
+// Coordinates, range test, floor and corner rows of one sample (Sec. 3: the 2x2 neighbourhood)
+// at normalized location xy with attention weight a. h_im / w_im are formed with one fp32
+// rounding, so floor() decisions are reproducible.
+__device__ __forceinline__ void describe_at(const Params& p, const int* s_lvl, int n, int m, int k, float2 xy,
+                                            float a, bool fold_attn, SampleDesc& sd) {
     sd.off = make_int4(kOOBElem, kOOBElem, kOOBElem, kOOBElem);
     sd.w = make_float4(0.f, 0.f, 0.f, 0.f);
     sd.a = 0.f;
     sd.lh = 0.f;
     sd.lw = 0.f;
-    if (q >= p.Lq) return;
     const int l = k / p.P;
     const int H = s_lvl[l], W = s_lvl[kMaxLevels + l], st = s_lvl[2 * kMaxLevels + l];
-    const int smp = ((n * p.Lq + q) * p.M + m) * p.K + k;
-    const float2 xy = reinterpret_cast<const float2*>(p.loc)[smp];
-    const float a = p.attn[smp];
     const float Hf = (float)H, Wf = (float)W;
     const float w_im = __builtin_fmaf(xy.x, Wf, -0.5f);
     const float h_im = __builtin_fmaf(xy.y, Hf, -0.5f);
@@ -221,6 +229,29 @@ __device__ __forceinline__ void describe(const Params& p, const int* s_lvl, int 
     sd.off.y = (top && rig) ? base + step_w : (int)kOOBElem;
     sd.off.z = (bot && lef) ? base + step_h : (int)kOOBElem;
     sd.off.w = (bot && rig) ? base + step_h + step_w : (int)kOOBElem;
+}
+
+// The sample k of query q with its location and weight read from sampling_loc / attn_weight.
+__device__ __forceinline__ void describe(const Params& p, const int* s_lvl, int n, int m, int q, int k,
+                                         bool fold_attn, SampleDesc& sd) {
+    if (q >= p.Lq) {
+        describe_at(p, s_lvl, n, m, k, make_float2(-2.f, -2.f), 0.f, fold_attn, sd);  // off the map
+        return;
+    }
+    const int smp = ((n * p.Lq + q) * p.M + m) * p.K + k;
+    describe_at(p, s_lvl, n, m, k, reinterpret_cast<const float2*>(p.loc)[smp], p.attn[smp], fold_attn, sd);
+}
+
+// Location of sample k of query q from the layer's predictions (Sec. 4, first paragraph: the
+// coordinates come first): reference point on the level plus the offset divided by the level size,
+// the division and then the addition each rounded once in fp32.
+__device__ __forceinline__ float2 fused_location(const Params& p, const int* s_lvl, int n, int m, int q, int k) {
+    const int l = k / p.P;
+    const int smp = ((n * p.Lq + q) * p.M + m) * p.K + k;
+    const float2 o = reinterpret_cast<const float2*>(p.pix_offsets)[smp];
+    const float2 r = reinterpret_cast<const float2*>(p.ref)[(n * p.Lq + q) * p.L + l];
+    const float fx = o.x / (float)s_lvl[kMaxLevels + l], fy = o.y / (float)s_lvl[l];
+    return make_float2(r.x + fx, r.y + fy);
 }
 
 __device__ __forceinline__ void load_levels(const Params& p, int* s_lvl) {

@@ -21,12 +21,15 @@
 namespace msda {
 namespace {
 
-template <typename T, int VEC, int LPP>
+// FUSED: the locations and weights are computed from ref / offsets / logits (the softmax over a
+// query's L*P logits is reduced over the query's lanes first).
+template <typename T, int VEC, int LPP, bool FUSED>
 __global__ __launch_bounds__(kBlock) void fwd_kernel(Params p) {
     constexpr int PPW = 64 / LPP;
     __shared__ int s_lvl[3 * kMaxLevels];
     __shared__ int4 s_off[kWaves][kMaxItems];
     __shared__ float4 s_w[kWaves][kMaxItems];
+    __shared__ float2 s_stat[kWaves][FUSED ? PPW : 1];  // (max logit, 1 / sum of exponentials)
     load_levels(p, s_lvl);
 
     Tile t;
@@ -38,6 +41,17 @@ __global__ __launch_bounds__(kBlock) void fwd_kernel(Params p) {
     const int KC = K < kMaxItems / PPW ? K : kMaxItems / PPW;
     const rsrc_t vr = make_rsrc(p.value, p.value_bytes);
     T* out = static_cast<T*>(p.out);
+    if constexpr (FUSED) {
+        const int q = q_mine < p.Lq ? q_mine : p.Lq - 1;
+        const float* z = p.logits + ((size_t)(t.n * p.Lq + q) * p.M + t.m) * K;
+        float mx = -INFINITY;
+        for (int k = sub; k < K; k += LPP) mx = fmaxf(mx, z[k]);
+        mx = group_max<LPP>(mx);
+        float sum = 0.f;
+        for (int k = sub; k < K; k += LPP) sum += expf(z[k] - mx);
+        sum = group_sum<LPP>(sum);
+        if (sub == 0) s_stat[wave][ps] = make_float2(mx, 1.f / sum);
+    }
 
     for (int c0 = 0; c0 < p.D; c0 += LPP * VEC) {
         const int chan = c0 + sub * VEC;
@@ -53,7 +67,19 @@ __global__ __launch_bounds__(kBlock) void fwd_kernel(Params p) {
             for (int j = lane; j < PPW * kn; j += 64) {
                 const int jq = j / kn, jk = j - jq * kn;
                 SampleDesc sd;
-                describe(p, s_lvl, t.n, t.m, t.q0 + jq, k0 + jk, true, sd);
+                if constexpr (FUSED) {
+                    const int q = t.q0 + jq, k = k0 + jk;
+                    if (q < p.Lq) {
+                        const float2 st = s_stat[wave][jq];
+                        const float z = p.logits[((size_t)(t.n * p.Lq + q) * p.M + t.m) * K + k];
+                        describe_at(p, s_lvl, t.n, t.m, k, fused_location(p, s_lvl, t.n, t.m, q, k),
+                                    expf(z - st.x) * st.y, true, sd);
+                    } else {
+                        describe_at(p, s_lvl, t.n, t.m, k, make_float2(-2.f, -2.f), 0.f, true, sd);
+                    }
+                } else {
+                    describe(p, s_lvl, t.n, t.m, t.q0 + jq, k0 + jk, true, sd);
+                }
                 s_off[wave][j] = sd.off;
                 s_w[wave][j] = sd.w;
             }
@@ -82,13 +108,22 @@ __global__ __launch_bounds__(kBlock) void fwd_kernel(Params p) {
 
 template <typename T, int VEC, int LPP>
 struct FwdK {
-    static auto fn() { return fwd_kernel<T, VEC, LPP>; }
+    static auto fn() { return fwd_kernel<T, VEC, LPP, false>; }
+};
+template <typename T, int VEC, int LPP>
+struct FwdFusedK {
+    static auto fn() { return fwd_kernel<T, VEC, LPP, true>; }
 };
 
 }  // namespace
 
 hipError_t launch_forward(const Params& p, msda_dtype_t dtype, hipStream_t stream) {
     return dtype == MSDA_F16 ? launch_typed<FwdK, _Float16>(p, stream) : launch_typed<FwdK, float>(p, stream);
+}
+
+hipError_t launch_forward_fused(const Params& p, msda_dtype_t dtype, hipStream_t stream) {
+    return dtype == MSDA_F16 ? launch_typed<FwdFusedK, _Float16>(p, stream)
+                             : launch_typed<FwdFusedK, float>(p, stream);
 }
 
 }  // namespace msda

@@ -31,6 +31,9 @@ struct Params {
     const void* value;     // [n_batch, S, M, D] dtype (already offset to the first batch item)
     const float* loc;      // [n_batch, Lq, M, L, P, 2]
     const float* attn;     // [n_batch, Lq, M, L, P]
+    const float* ref;      // [n_batch, Lq, L, 2]          (fused entry points)
+    const float* pix_offsets;  // [n_batch, Lq, M, L, P, 2] (fused entry points, pixels)
+    const float* logits;   // [n_batch, Lq, M, L*P]        (fused entry points)
     void* out;             // [n_batch, Lq, M*D] dtype                       (forward)
     const void* grad_out;  // [n_batch, Lq, M*D] dtype                       (backward)
     float* grad_value;     // [n_batch, S, M, D] fp32                        (backward)
@@ -67,6 +70,14 @@ struct Params {
 };
 
 hipError_t launch_forward(const Params& p, msda_dtype_t dtype, hipStream_t stream);
+// The forward with locations and weights computed from ref / offsets / logits.
+hipError_t launch_forward_fused(const Params& p, msda_dtype_t dtype, hipStream_t stream);
+// loc and attn of every sample from ref / offsets / logits (the backward's prologue).
+hipError_t launch_prologue(const Params& p, float* loc, float* attn, hipStream_t stream);
+// grad_offsets, grad_logits and (if non-null) grad_ref from the sampling's grad_loc / grad_attn.
+hipError_t launch_prologue_grad(const Params& p, const float* attn, const float* grad_loc,
+                                const float* grad_attn, float* grad_offsets, float* grad_logits,
+                                float* grad_ref, hipStream_t stream);
 // grad_loc / grad_attn; with `atomic_grad_value` the same kernel also scatters grad_value with
 // fp32 atomics (grad_value must be zero beforehand).
 hipError_t launch_backward_grads(const Params& p, msda_dtype_t dtype, bool atomic_grad_value, hipStream_t stream);

@@ -26,6 +26,7 @@ MSDA_WORKSPACE_PREFERRED = 0
 MSDA_WORKSPACE_OWNER = 1
 
 EXPORTED = ["msda_check_args", "msda_forward", "msda_backward", "msda_backward_workspace_size",
+            "msda_forward_fused", "msda_backward_fused_workspace_size", "msda_backward_fused",
             "msda_status_string", "msda_last_error", "msda_version"]
 
 
@@ -56,6 +57,13 @@ def lib():
         L.msda_backward_workspace_size.argtypes = [ip, ip] + [i64] * 7 + [ctypes.c_int, ctypes.c_int,
                                                                          ctypes.POINTER(ctypes.c_size_t)]
         L.msda_backward_workspace_size.restype = ctypes.c_int
+        L.msda_forward_fused.argtypes = [vp, ip, ip, vp, vp, vp, vp] + [i64] * 7 + [ctypes.c_int, vp]
+        L.msda_forward_fused.restype = ctypes.c_int
+        L.msda_backward_fused_workspace_size.argtypes = L.msda_backward_workspace_size.argtypes
+        L.msda_backward_fused_workspace_size.restype = ctypes.c_int
+        L.msda_backward_fused.argtypes = [vp, ip, ip] + [vp] * 9 + [ctypes.c_size_t] + [i64] * 7 + \
+            [ctypes.c_int, vp]
+        L.msda_backward_fused.restype = ctypes.c_int
         L.msda_status_string.argtypes = [ctypes.c_int]
         L.msda_status_string.restype = ctypes.c_char_p
         L.msda_last_error.argtypes = []
@@ -196,6 +204,83 @@ def backward(value, spatial_shapes, level_start_index, sampling_loc, attn_weight
     return grad_value, grad_loc, grad_attn
 
 
+def _fused_dims(value, ref_points, offsets, logits):
+    N, S, M, D = value.shape
+    if offsets.dim() != 6 or offsets.shape[-1] != 2:
+        raise ValueError(f"offsets must be [N, Lq, M, L, P, 2], not {tuple(offsets.shape)}")
+    _, Lq, M2, L, P, _ = offsets.shape
+    if (M2 != M or tuple(ref_points.shape) != (N, Lq, L, 2) or tuple(logits.shape) != (N, Lq, M, L * P)
+            or offsets.shape[0] != N):
+        raise ValueError(f"value {tuple(value.shape)}, ref_points {tuple(ref_points.shape)}, offsets "
+                         f"{tuple(offsets.shape)} and logits {tuple(logits.shape)} do not match")
+    return N, S, M, D, Lq, L, P
+
+
+def fused_workspace_size(spatial_shapes, level_start_index, N, S, M, D, Lq, L, P, dtype,
+                         mode: int = MSDA_WORKSPACE_PREFERRED) -> int:
+    """msda_backward_fused_workspace_size: staging of the locations, weights and their gradients
+    plus the owner-computes workspace (as workspace_size with the same mode)."""
+    sh, st = _host_tables(spatial_shapes, level_start_index)
+    out = ctypes.c_size_t(0)
+    r = lib().msda_backward_fused_workspace_size(_iptr(sh), _iptr(st), N, S, M, D, Lq, L, P, int(dtype),
+                                                 int(mode), ctypes.byref(out))
+    _raise(r, "msda_backward_fused_workspace_size")
+    return int(out.value)
+
+
+def forward_fused(value, spatial_shapes, level_start_index, ref_points, offsets, logits, out=None, stream=None):
+    """out[N, Lq, M*D] from msda_forward_fused: locations ref_points + offsets / (W_l, H_l) and
+    weights softmax(logits) are formed inside the kernel."""
+    import torch
+
+    N, S, M, D, Lq, L, P = _fused_dims(value, ref_points, offsets, logits)
+    if out is None:
+        out = torch.empty((N, Lq, M * D), dtype=value.dtype, device=value.device)
+    sh, st = _host_tables(spatial_shapes, level_start_index)
+    r = lib().msda_forward_fused(_dptr(value), _iptr(sh), _iptr(st), _dptr(ref_points), _dptr(offsets),
+                                 _dptr(logits), _dptr(out), N, S, M, D, Lq, L, P, _dtype_code(value),
+                                 _stream(stream))
+    _raise(r, "msda_forward_fused")
+    return out
+
+
+def backward_fused(value, spatial_shapes, level_start_index, ref_points, offsets, logits, grad_out,
+                   grad_value=None, grad_ref=None, grad_offsets=None, grad_logits=None, workspace="auto",
+                   want_grad_ref: bool = True, stream=None):
+    """(grad_value fp32, grad_ref or None, grad_offsets, grad_logits) from msda_backward_fused.
+
+    workspace: "auto" (the size the library prefers), "owner" (with the owner-computes grad_value
+    wherever it applies) or a caller-owned uint8 device tensor of at least the staging size.
+    """
+    import torch
+
+    N, S, M, D, Lq, L, P = _fused_dims(value, ref_points, offsets, logits)
+    dev = value.device
+    if grad_value is None:
+        grad_value = torch.empty((N, S, M, D), dtype=torch.float32, device=dev)
+    if grad_ref is None and want_grad_ref:
+        grad_ref = torch.empty(tuple(ref_points.shape), dtype=torch.float32, device=dev)
+    if grad_offsets is None:
+        grad_offsets = torch.empty(tuple(offsets.shape), dtype=torch.float32, device=dev)
+    if grad_logits is None:
+        grad_logits = torch.empty(tuple(logits.shape), dtype=torch.float32, device=dev)
+    sh, st = _host_tables(spatial_shapes, level_start_index)
+    if isinstance(workspace, str):
+        if workspace not in ("auto", "owner"):
+            raise ValueError(f"workspace must be 'auto', 'owner' or a tensor, not {workspace!r}")
+        mode = MSDA_WORKSPACE_PREFERRED if workspace == "auto" else MSDA_WORKSPACE_OWNER
+        nbytes = fused_workspace_size(sh.reshape(-1, 2), st, N, S, M, D, Lq, L, P, _dtype_code(value), mode)
+        workspace = torch.empty(max(nbytes, 1), dtype=torch.uint8, device=dev)
+    ws_bytes = workspace.numel() * workspace.element_size()
+    r = lib().msda_backward_fused(_dptr(value), _iptr(sh), _iptr(st), _dptr(ref_points), _dptr(offsets),
+                                  _dptr(logits), _dptr(grad_out), _dptr(grad_value),
+                                  _dptr(grad_ref) if grad_ref is not None else None, _dptr(grad_offsets),
+                                  _dptr(grad_logits), _dptr(workspace), ws_bytes, N, S, M, D, Lq, L, P,
+                                  _dtype_code(value), _stream(stream))
+    _raise(r, "msda_backward_fused")
+    return grad_value, grad_ref, grad_offsets, grad_logits
+
+
 def forward_raw(value_ptr: int, shapes: np.ndarray, starts: np.ndarray, loc_ptr: int, attn_ptr: int,
                 out_ptr: int, dims: Sequence[int], dtype: int, stream: int) -> int:
     """msda_forward on raw device addresses; returns the status (used by the benchmark loop)."""
@@ -209,3 +294,20 @@ def backward_raw(value_ptr: int, shapes: np.ndarray, starts: np.ndarray, loc_ptr
     """msda_backward on raw device addresses; returns the status (used by the benchmark loop)."""
     return lib().msda_backward(value_ptr, _iptr(shapes), _iptr(starts), loc_ptr, attn_ptr, gout_ptr,
                                gv_ptr, gl_ptr, ga_ptr, ws_ptr, ws_bytes, *dims, dtype, stream)
+
+
+def forward_fused_raw(value_ptr: int, shapes: np.ndarray, starts: np.ndarray, ref_ptr: int, off_ptr: int,
+                      logit_ptr: int, out_ptr: int, dims: Sequence[int], dtype: int, stream: int) -> int:
+    """msda_forward_fused on raw device addresses; returns the status (used by the benchmark loop)."""
+    return lib().msda_forward_fused(value_ptr, _iptr(shapes), _iptr(starts), ref_ptr, off_ptr, logit_ptr, out_ptr,
+                                    *dims, dtype, stream)
+
+
+def backward_fused_raw(value_ptr: int, shapes: np.ndarray, starts: np.ndarray, ref_ptr: int, off_ptr: int,
+                       logit_ptr: int, gout_ptr: int, gv_ptr: int, gref_ptr: Optional[int], goff_ptr: int,
+                       glog_ptr: int, ws_ptr: int, ws_bytes: int, dims: Sequence[int], dtype: int,
+                       stream: int) -> int:
+    """msda_backward_fused on raw device addresses; returns the status (used by the benchmark loop)."""
+    return lib().msda_backward_fused(value_ptr, _iptr(shapes), _iptr(starts), ref_ptr, off_ptr, logit_ptr,
+                                     gout_ptr, gv_ptr, gref_ptr, goff_ptr, glog_ptr, ws_ptr, ws_bytes, *dims,
+                                     dtype, stream)

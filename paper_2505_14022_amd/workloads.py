@@ -195,6 +195,49 @@ def generate(w: Workload, seed: Optional[int] = None) -> Inputs:
                   grad_out=np.ascontiguousarray(grad_out))
 
 
+@dataclass
+class FusedInputs:
+    """Raw layer predictions for the fused entry points: the locations and weights are computed
+    from them inside the operation."""
+    w: Workload
+    value: np.ndarray  # [N,S,M,D] float32 or float16
+    shapes: np.ndarray  # [L,2] int64
+    starts: np.ndarray  # [L] int64
+    ref: np.ndarray  # [N,Lq,L,2] float32, normalized (x, y) per level
+    offsets: np.ndarray  # [N,Lq,M,L,P,2] float32, pixels of the sampled level
+    logits: np.ndarray  # [N,Lq,M,L*P] float32
+    grad_out: np.ndarray  # [N,Lq,M*D] float32 or float16
+
+
+def generate_fused(w: Workload, seed: Optional[int] = None) -> FusedInputs:
+    """Draw raw predictions of workload ``w``: the same reference points as :func:`generate` (one
+    normalized point per query, used on every level; uniform when the workload has none), offsets
+    ~ N(0, offset_px) pixels (2 px for workloads without an offset scale) and N(0,1) logits."""
+    rng = np.random.default_rng(SEED_BASE + 1000 + w.index if seed is None else seed)
+    N, M, D, L, P, Lq, S = w.N, w.M, w.D, w.L, w.P, w.Lq, w.S
+    shapes = w.shapes_array()
+    value = rng.standard_normal((N, S, M, D), dtype=np.float32)
+    if w.refs in ("uniform_loc", "uniform"):
+        ref = rng.uniform(w.ref_lo, w.ref_hi, size=(N, Lq, 2)).astype(np.float32)
+    elif w.refs in ("own_pixel", "bev_grid"):
+        r = _own_pixel_refs(w.shapes)
+        assert r.shape[0] == Lq, "pixel-centre references need Lq == S"
+        ref = np.broadcast_to(r[None].astype(np.float32), (N, Lq, 2))
+    else:
+        raise ValueError(w.refs)
+    ref = np.ascontiguousarray(np.broadcast_to(ref[:, :, None, :], (N, Lq, L, 2)))
+    offsets = rng.standard_normal((N, Lq, M, L, P, 2), dtype=np.float32)
+    offsets *= np.float32(w.offset_px if w.offset_px > 0 else 2.0)
+    logits = rng.standard_normal((N, Lq, M, L * P), dtype=np.float32)
+    grad_out = rng.standard_normal((N, Lq, M * D), dtype=np.float32)
+    if w.dtype == "f16":
+        value = _to_f16(value)
+        grad_out = _to_f16(grad_out)
+    return FusedInputs(w=w, value=np.ascontiguousarray(value), shapes=shapes, starts=w.starts(), ref=ref,
+                       offsets=np.ascontiguousarray(offsets), logits=np.ascontiguousarray(logits),
+                       grad_out=np.ascontiguousarray(grad_out))
+
+
 def random_case(N: int, M: int, D: int, shapes, P: int, Lq: int, dtype: str = "f32", seed: int = 0,
                 lo: float = -0.1, hi: float = 1.1) -> Inputs:
     """A generic random problem: value ~ N(0,1), locations ~ U(lo, hi) per coordinate (so a share

@@ -116,3 +116,58 @@ def check_parity(inp: workloads.Inputs, backward: bool = True, gpu=None, ref=Non
                                  f"gpu {float(gpu[k][i]):.6g} ref {float(ref[k][i]):.6g}; {nbad} of {d.size} "
                                  f"elements off; <gpu,ref>/<ref,ref> = {ratio:.4f}")
     return errs
+
+
+# The fused entry points' extra outputs: grad_offsets = grad_loc / (W, H) keeps grad_loc's
+# relative error; grad_logits and grad_ref are short fp32 sums of grad_attn / grad_loc terms.
+TOL_GRAD_OFFSETS = 1e-3
+TOL_GRAD_LOGITS = 1e-3
+TOL_GRAD_REF = 1e-3
+
+
+def run_gpu_fused(inp: workloads.FusedInputs, workspace="auto", want_grad_ref: bool = True):
+    import torch
+
+    dev = torch.device("cuda:0")
+    t = {k: torch.from_numpy(getattr(inp, k)).to(dev) for k in ("value", "ref", "offsets", "logits", "grad_out")}
+    out = msda.forward_fused(t["value"], inp.shapes, inp.starts, t["ref"], t["offsets"], t["logits"])
+    gv, gref, goff, glog = msda.backward_fused(t["value"], inp.shapes, inp.starts, t["ref"], t["offsets"],
+                                               t["logits"], t["grad_out"], workspace=workspace,
+                                               want_grad_ref=want_grad_ref)
+    torch.cuda.synchronize()
+    res = {"out": out.cpu().numpy(), "grad_value": gv.cpu().numpy(), "grad_offsets": goff.cpu().numpy(),
+           "grad_logits": glog.cpu().numpy()}
+    if gref is not None:
+        res["grad_ref"] = gref.cpu().numpy()
+    return res
+
+
+def run_oracle_fused(inp: workloads.FusedInputs):
+    out = oracle.forward_fused(inp.value, inp.shapes, inp.starts, inp.ref, inp.offsets, inp.logits)
+    gv, goff, glog, gref = oracle.backward_fused(inp.value, inp.shapes, inp.starts, inp.ref, inp.offsets,
+                                                 inp.logits, inp.grad_out)
+    return {"out": out, "grad_value": gv, "grad_offsets": goff, "grad_logits": glog, "grad_ref": gref}
+
+
+def check_parity_fused(inp: workloads.FusedInputs, workspace="auto", want_grad_ref: bool = True):
+    fp16 = inp.value.dtype == np.float16
+    gpu = run_gpu_fused(inp, workspace, want_grad_ref)
+    ref = run_oracle_fused(inp)
+    tols = {"out": TOL_OUT_F16 if fp16 else TOL_OUT_F32, "grad_value": TOL_GRAD_VALUE,
+            "grad_offsets": TOL_GRAD_OFFSETS, "grad_logits": TOL_GRAD_LOGITS, "grad_ref": TOL_GRAD_REF}
+    if not want_grad_ref:
+        del tols["grad_ref"]
+        assert "grad_ref" not in gpu
+    errs = {}
+    for k, t in tols.items():
+        assert gpu[k].shape == tuple(ref[k].shape), f"{k}: shape {gpu[k].shape} vs {ref[k].shape}"
+        assert np.all(np.isfinite(gpu[k])), f"{inp.w.name}: non-finite values in {k}"
+        errs[k] = normwise(gpu[k], ref[k])
+    say(f"  {inp.w.name} (fused): " + ", ".join(f"{k} {errs[k]:.2e} (tol {tols[k]:.0e})" for k in errs))
+    for k, t in tols.items():
+        if errs[k] > t:
+            d = np.abs(gpu[k].astype(np.float64) - ref[k])
+            i = np.unravel_index(int(np.argmax(d)), d.shape)
+            raise AssertionError(f"{inp.w.name}: {k} normwise error {errs[k]:.3e} > {t:.0e}; worst at {i}: "
+                                 f"gpu {float(gpu[k][i]):.6g} ref {float(ref[k][i]):.6g}")
+    return errs

@@ -185,3 +185,48 @@ def test_workspace_size_not_applicable(L):
     a = base()
     a[6] = 0  # nothing to do
     assert msda.workspace_size(a[0], a[1], *a[2:9], a[9]) == 0
+
+
+@pytest.mark.parametrize("w", workloads.WORKLOADS, ids=lambda w: w.name)
+def test_fused_workspace_sizes(L, w):
+    # staging of loc (8 B), attn (4 B), grad_loc (8 B) and grad_attn (4 B) per sample of one launch,
+    # each rounded to 256 bytes, plus the plain backward's workspace of the same mode
+    staging = msda.fused_workspace_size(*_args(w)) - msda.workspace_size(*_args(w))
+    assert 24 * w.samples <= staging < 24 * w.samples + 4 * 256, staging
+    owner = msda.fused_workspace_size(*_args(w), msda.MSDA_WORKSPACE_OWNER)
+    assert owner == staging + msda.workspace_size(*_args(w), msda.MSDA_WORKSPACE_OWNER)
+
+
+def test_fused_forward_checks_pointers_before_launching(L):
+    a = base()
+    ip = ctypes.POINTER(ctypes.c_int64)
+
+    def fwd(ptrs, a):
+        return L.msda_forward_fused(ptrs[0], a[0].ctypes.data_as(ip), a[1].ctypes.data_as(ip), *ptrs[1:],
+                                    *a[2:9], a[9], None)
+
+    assert fwd([None] * 5, a) == msda.MSDA_ERROR_INVALID_VALUE
+    # offsets must be 8-byte aligned
+    assert fwd([0x1000, 0x2000, 0x3004, 0x4000, 0x5000], a) == msda.MSDA_ERROR_INVALID_VALUE
+    assert "misaligned" in msda.last_error()
+    a[6] = 0  # Lq = 0: a no-op
+    assert fwd([None] * 5, a) == msda.MSDA_SUCCESS
+
+
+def test_fused_backward_needs_its_workspace(L):
+    a = base()
+    ip = ctypes.POINTER(ctypes.c_int64)
+
+    def bwd(ws, ws_bytes, a, grad_ref=0xa000):
+        return L.msda_backward_fused(0x1000, a[0].ctypes.data_as(ip), a[1].ctypes.data_as(ip), 0x2000, 0x3000,
+                                     0x4000, 0x5000, 0x6000, grad_ref, 0x7000, 0x8000, ws, ws_bytes, *a[2:9],
+                                     a[9], None)
+
+    need = msda.fused_workspace_size(a[0], a[1], *a[2:9], a[9])
+    assert need > 0
+    assert bwd(None, 0, a) == msda.MSDA_ERROR_INVALID_VALUE and "workspace" in msda.last_error()
+    assert bwd(0x10000, need - 1, a) == msda.MSDA_ERROR_INVALID_VALUE and "workspace" in msda.last_error()
+    assert bwd(0x10010, need, a) == msda.MSDA_ERROR_INVALID_VALUE and "aligned" in msda.last_error()
+    # grad_ref is optional, but a given one must be 8-byte aligned
+    assert bwd(0x10000, need, a, grad_ref=0xa004) == msda.MSDA_ERROR_INVALID_VALUE
+    assert "misaligned" in msda.last_error()
