@@ -1,6 +1,6 @@
 """Benchmark: MSDA forward + backward (one training step of the operator) on one MI355X.
 
-    python bench.py [--steps K] [--warmup W] [--workload detr_encoder] [--no-cpu-baseline]
+    python bench.py [--steps K] [--warmup W] [--workload detr_encoder] [--no-cpu-baseline] [--fused]
 
 A step is msda_forward followed by msda_backward on one batch of seeded synthetic inputs that
 are resident in HBM before the timed region starts. K steps are timed between two device
@@ -14,6 +14,9 @@ counted for the same sources (FETCH_SIZE and WRITE_SIZE, scaled by a plain copy 
 read from profiles/traffic_<workload>.txt when its source hash matches, else null. A 1 GiB
 device copy gives the achievable bandwidth beside the published peak. The CPU baseline is the
 plain oracle timed on this host.
+
+--fused times msda_forward_fused + msda_backward_fused instead: the step then starts from
+reference points, pixel offsets and attention logits, and ends with their gradients.
 """
 from __future__ import annotations
 
@@ -115,36 +118,54 @@ def touched_rows(inp: workloads.Inputs) -> int:
     return int(np.unique(np.concatenate(keys)).size)
 
 
-def compulsory_bytes(inp: workloads.Inputs):
-    """Bytes the forward and backward passes must move at least once (HBM)."""
+class _Locations:
+    """The sampling locations of fused inputs, for touched_rows only (fp32: ref + offset / size)."""
+
+    def __init__(self, f: workloads.FusedInputs):
+        self.w, self.shapes, self.starts = f.w, f.shapes, f.starts
+        size = np.asarray([[W, H] for H, W in f.shapes], dtype=np.float32)  # [L, 2] as (x, y)
+        self.loc = f.ref[:, :, None, :, None, :] + f.offsets / size[None, None, None, :, None, :]
+
+
+def compulsory_bytes(inp, fused: bool = False):
+    """Bytes the forward and backward passes must move at least once (HBM). Fused: the inputs are
+    offsets (8 B), logits (4 B) and reference points instead of locations and weights, and the
+    backward writes their gradients instead."""
     w = inp.w
     T = w.samples
     es = 2 if w.dtype == "f16" else 4
-    rows = touched_rows(inp)
+    rows = touched_rows(_Locations(inp) if fused else inp)
     touched = rows * w.D * es
     io = w.N * w.Lq * w.M * w.D * es
-    fwd = touched + T * 8 + T * 4 + io
-    bwd = touched + T * 8 + T * 4 + io + w.N * w.S * w.M * w.D * 4 + T * 8 + T * 4
+    ref = w.N * w.Lq * w.L * 8 if fused else 0
+    fwd = touched + T * 8 + T * 4 + ref + io
+    bwd = touched + T * 8 + T * 4 + ref + io + w.N * w.S * w.M * w.D * 4 + T * 8 + T * 4 + ref
     return fwd, bwd, rows
 
 
-def cpu_baseline(inp: workloads.Inputs, budget_s: float = 10.0):
+def cpu_baseline(inp, budget_s: float = 10.0, fused: bool = False):
     """The oracle's full forward+backward step, repeated for about `budget_s` seconds."""
     import oracle
 
     steps, th = 0, 0
     t0 = time.perf_counter()
     while True:
-        _, th = oracle.forward(inp.value, inp.shapes, inp.starts, inp.loc, inp.attn, return_threads=True)
-        oracle.backward(inp.value, inp.shapes, inp.starts, inp.loc, inp.attn, inp.grad_out)
+        if fused:
+            loc, attn = oracle.prologue(inp.ref, inp.offsets, inp.logits, inp.shapes)
+            _, th = oracle.forward(inp.value, inp.shapes, inp.starts, loc, attn, return_threads=True)
+            oracle.backward_fused(inp.value, inp.shapes, inp.starts, inp.ref, inp.offsets, inp.logits,
+                                  inp.grad_out)
+        else:
+            _, th = oracle.forward(inp.value, inp.shapes, inp.starts, inp.loc, inp.attn, return_threads=True)
+            oracle.backward(inp.value, inp.shapes, inp.starts, inp.loc, inp.attn, inp.grad_out)
         steps += 1
         dt = time.perf_counter() - t0
         if dt >= budget_s or (steps >= 1 and dt * (steps + 1) / steps > 3 * budget_s):
             break
     return {"value": round(inp.w.samples * steps / dt / 1e9, 6), "unit": "Gsamples/s", "cores": int(th),
             "kind": "oracle", "seconds": round(dt, 3),
-            "sample": f"{steps} full forward+backward steps of the {inp.w.name} workload "
-                      f"({inp.w.samples} samples each), fp64 oracle, OpenMP threads={th}"}
+            "sample": f"{steps} full {'fused ' if fused else ''}forward+backward steps of the {inp.w.name} "
+                      f"workload ({inp.w.samples} samples each), fp64 oracle, OpenMP threads={th}"}
 
 
 def main():
@@ -157,6 +178,9 @@ def main():
     ap.add_argument("--no-compulsory", action="store_true", help="skip counting touched rows (faster)")
     ap.add_argument("--atomic-grad-value", action="store_true",
                     help="pass no workspace, so msda_backward accumulates grad_value with fp32 atomics")
+    ap.add_argument("--fused", action="store_true",
+                    help="time msda_forward_fused + msda_backward_fused (inputs: reference points, pixel offsets, "
+                         "logits)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="instead of the benchmark, copy a MIB-mebibyte fp32 buffer 5 times (a plain copy kernel of "
                          "known size, used to scale FETCH_SIZE / WRITE_SIZE counters)")
@@ -184,37 +208,63 @@ def main():
 
     w = workloads.BY_NAME[args.workload]
     print(f"[bench] generating {w.name}", file=sys.stderr, flush=True)
-    inp = workloads.generate(w)
+    inp = workloads.generate_fused(w) if args.fused else workloads.generate(w)
     dev = torch.device("cuda:0")
-    value = torch.from_numpy(inp.value).to(dev)
-    loc = torch.from_numpy(inp.loc).to(dev)
-    attn = torch.from_numpy(inp.attn).to(dev)
-    gout = torch.from_numpy(inp.grad_out).to(dev)
+
+    def dev_in(a):
+        return torch.from_numpy(a).to(dev)
+
+    value = dev_in(inp.value)
+    gout = dev_in(inp.grad_out)
     out = torch.empty((w.N, w.Lq, w.M * w.D), dtype=value.dtype, device=dev)
     gv = torch.empty(tuple(value.shape), dtype=torch.float32, device=dev)
-    gl = torch.empty(tuple(loc.shape), dtype=torch.float32, device=dev)
-    ga = torch.empty(tuple(attn.shape), dtype=torch.float32, device=dev)
     stream = torch.cuda.current_stream()
     sp = stream.cuda_stream
     dims = (w.N, w.S, w.M, w.D, w.Lq, w.L, w.P)
     dt = msda.MSDA_F16 if w.dtype == "f16" else msda.MSDA_F32
     shapes = np.ascontiguousarray(inp.shapes.reshape(-1))
     starts = np.ascontiguousarray(inp.starts)
-    ws_bytes = 0 if args.atomic_grad_value else msda.workspace_size(inp.shapes, inp.starts, *dims, dt)
-    ws = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device=dev)
-    P_ = (value.data_ptr(), loc.data_ptr(), attn.data_ptr(), gout.data_ptr(), out.data_ptr(), gv.data_ptr(),
-          gl.data_ptr(), ga.data_ptr(), ws.data_ptr() if ws_bytes else None)
+    if args.fused:
+        ref, off, logit = dev_in(inp.ref), dev_in(inp.offsets), dev_in(inp.logits)
+        gref, goff, glog = (torch.empty(tuple(t.shape), dtype=torch.float32, device=dev) for t in (ref, off, logit))
+        plain = msda.workspace_size(inp.shapes, inp.starts, *dims, dt)
+        staging = msda.fused_workspace_size(inp.shapes, inp.starts, *dims, dt) - plain
+        binned_bytes = 0 if args.atomic_grad_value else plain  # without it: grad_value by atomics
+        ws_bytes = staging + binned_bytes
+        ws = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device=dev)
 
-    def fwd():
-        r = msda.forward_raw(P_[0], shapes, starts, P_[1], P_[2], P_[4], dims, dt, sp)
-        if r:
-            raise msda.MsdaError(r, "msda_forward", msda.last_error())
+        def fwd():
+            r = msda.forward_fused_raw(value.data_ptr(), shapes, starts, ref.data_ptr(), off.data_ptr(),
+                                       logit.data_ptr(), out.data_ptr(), dims, dt, sp)
+            if r:
+                raise msda.MsdaError(r, "msda_forward_fused", msda.last_error())
 
-    def bwd():
-        r = msda.backward_raw(P_[0], shapes, starts, P_[1], P_[2], P_[3], P_[5], P_[6], P_[7], P_[8], ws_bytes,
-                              dims, dt, sp)
-        if r:
-            raise msda.MsdaError(r, "msda_backward", msda.last_error())
+        def bwd():
+            r = msda.backward_fused_raw(value.data_ptr(), shapes, starts, ref.data_ptr(), off.data_ptr(),
+                                        logit.data_ptr(), gout.data_ptr(), gv.data_ptr(), gref.data_ptr(),
+                                        goff.data_ptr(), glog.data_ptr(), ws.data_ptr(), ws_bytes, dims, dt, sp)
+            if r:
+                raise msda.MsdaError(r, "msda_backward_fused", msda.last_error())
+    else:
+        loc, attn = dev_in(inp.loc), dev_in(inp.attn)
+        gl = torch.empty(tuple(loc.shape), dtype=torch.float32, device=dev)
+        ga = torch.empty(tuple(attn.shape), dtype=torch.float32, device=dev)
+        ws_bytes = 0 if args.atomic_grad_value else msda.workspace_size(inp.shapes, inp.starts, *dims, dt)
+        binned_bytes = ws_bytes
+        ws = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device=dev)
+        P_ = (value.data_ptr(), loc.data_ptr(), attn.data_ptr(), gout.data_ptr(), out.data_ptr(), gv.data_ptr(),
+              gl.data_ptr(), ga.data_ptr(), ws.data_ptr() if ws_bytes else None)
+
+        def fwd():
+            r = msda.forward_raw(P_[0], shapes, starts, P_[1], P_[2], P_[4], dims, dt, sp)
+            if r:
+                raise msda.MsdaError(r, "msda_forward", msda.last_error())
+
+        def bwd():
+            r = msda.backward_raw(P_[0], shapes, starts, P_[1], P_[2], P_[3], P_[5], P_[6], P_[7], P_[8],
+                                  ws_bytes, dims, dt, sp)
+            if r:
+                raise msda.MsdaError(r, "msda_backward", msda.last_error())
 
     print(f"[bench] warmup {args.warmup}", file=sys.stderr, flush=True)
     for _ in range(args.warmup):
@@ -255,27 +305,30 @@ def main():
         "data": "synthetic",
         "config": {"workload": w.name, "N": w.N, "M": w.M, "D": w.D, "levels": [list(s) for s in w.shapes],
                    "S": w.S, "Lq": w.Lq, "P": w.P, "samples_per_step": T, "value_dtype": w.dtype,
-                   "parallelism": "single GPU"},
+                   "parallelism": "single GPU",
+                   "entry": "fused (reference points, offsets, logits)" if args.fused else "sampling_loc, attn_weight"},
         "fwd_ms_mean": round(float(fwd_ms.mean()), 5),
         "fwd_ms_median": round(float(np.median(fwd_ms)), 5),
         "bwd_ms_mean": round(float(bwd_ms.mean()), 5),
         "bwd_ms_median": round(float(np.median(bwd_ms)), 5),
-        "grad_value_path": "owner-computes (binned)" if ws_bytes else "atomic",
+        "grad_value_path": "owner-computes (binned)" if binned_bytes else "atomic",
         "workspace_bytes": int(ws_bytes),
     }
     if not args.no_compulsory:
         print("[bench] counting compulsory bytes", file=sys.stderr, flush=True)
-        fb, bb, rows = compulsory_bytes(inp)
+        fb, bb, rows = compulsory_bytes(inp, args.fused)
         bwd_s = float(bwd_ms.mean()) / 1e3
         fwd_s = float(fwd_ms.mean()) / 1e3
         achieved = bb / bwd_s / 1e9
         copy_gbs = copy_peak_gbs(torch)
-        res["roofline"] = {"bound": "hbm", "kernel": "msda_backward (all of its kernels, one call)",
+        bname = "msda_backward_fused" if args.fused else "msda_backward"
+        res["roofline"] = {"bound": "hbm", "kernel": f"{bname} (all of its kernels, one call)",
                            "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                           "frac": round(achieved / HBM_PEAK_GBS, 5), "traffic": measured_traffic(w.name),
+                           "frac": round(achieved / HBM_PEAK_GBS, 5), "traffic": None if args.fused else measured_traffic(w.name),
                            "algorithmic_bytes": int(bb), "launch_ms": round(float(bwd_ms.mean()), 5),
                            "copy_peak": round(copy_gbs, 1), "frac_of_copy_peak": round(achieved / copy_gbs, 5)}
-        res["fwd_roofline"] = {"bound": "hbm", "kernel": "msda_forward (fwd_kernel)",
+        res["fwd_roofline"] = {"bound": "hbm", "kernel": "msda_forward_fused (fwd_kernel)" if args.fused else
+                               "msda_forward (fwd_kernel)",
                                "achieved": round(fb / fwd_s / 1e9, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                                "frac": round(fb / fwd_s / 1e9 / HBM_PEAK_GBS, 5), "algorithmic_bytes": int(fb),
                                "launch_ms": round(fwd_s * 1e3, 5)}
@@ -283,7 +336,7 @@ def main():
         res["touched_value_rows"] = rows
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle", file=sys.stderr, flush=True)
-        res["cpu_baseline"] = cpu_baseline(inp)
+        res["cpu_baseline"] = cpu_baseline(inp, fused=args.fused)
     print(json.dumps(res), flush=True)
 
 

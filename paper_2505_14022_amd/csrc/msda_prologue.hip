@@ -11,47 +11,97 @@
 namespace msda {
 namespace {
 
-// One thread per (n, q, m): its K samples' locations and weights.
+// G lanes per (n, q, m) row (G a power of two, at most 64): lane g takes the row's samples
+// g, g + G, ... so that consecutive lanes touch consecutive samples; the softmax statistics and
+// the chain rule's dot product are reduced over the row's G lanes. Lanes past the last row keep
+// running (with neutral values) so the cross-lane reductions see every lane active.
+template <int G>
 __global__ __launch_bounds__(256) void prologue_kernel(Params p, float* loc, float* attn) {
     __shared__ int s_lvl[3 * kMaxLevels];
     load_levels(p, s_lvl);
-    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;  // (n, q, m)
-    if (i >= (int64_t)p.n_batch * p.Lq * p.M) return;
-    const int m = (int)(i % p.M), nq = (int)(i / p.M);
-    const int n = nq / p.Lq, q = nq - n * p.Lq;
+    const int64_t rows = (int64_t)p.n_batch * p.Lq * p.M;
+    const int64_t row = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) / G;
+    const int g = threadIdx.x % G;
+    const bool live = row < rows;
     const int K = p.K;
-    const float* z = p.logits + i * K;
+    const float* z = p.logits + row * K;
     float mx = -INFINITY;
-    for (int k = 0; k < K; ++k) mx = fmaxf(mx, z[k]);
+    for (int k = g; k < K; k += G)
+        if (live) mx = fmaxf(mx, z[k]);
+    mx = group_max<G>(mx);
     float sum = 0.f;
-    for (int k = 0; k < K; ++k) sum += expf(z[k] - mx);
+    for (int k = g; k < K; k += G)
+        if (live) sum += expf(z[k] - mx);
+    sum = group_sum<G>(sum);
+    if (!live) return;
     const float inv = 1.f / sum;
-    for (int k = 0; k < K; ++k) {
-        attn[i * K + k] = expf(z[k] - mx) * inv;
-        reinterpret_cast<float2*>(loc)[i * K + k] = fused_location(p, s_lvl, n, m, q, k);
+    const int m = (int)(row % p.M), nq = (int)(row / p.M);
+    const int n = nq / p.Lq, q = nq - n * p.Lq;
+    for (int k = g; k < K; k += G) {
+        attn[row * K + k] = expf(z[k] - mx) * inv;
+        reinterpret_cast<float2*>(loc)[row * K + k] = fused_location(p, s_lvl, n, m, q, k);
     }
 }
 
-// One thread per (n, q, m): grad_offsets and grad_logits of its K samples.
+// grad_offsets and grad_logits, G lanes per (n, q, m) row as above.
+template <int G>
 __global__ __launch_bounds__(256) void prologue_grad_kernel(Params p, const float* attn, const float* grad_loc,
                                                              const float* grad_attn, float* grad_offsets,
                                                              float* grad_logits) {
     __shared__ int s_lvl[3 * kMaxLevels];
     load_levels(p, s_lvl);
-    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (i >= (int64_t)p.n_batch * p.Lq * p.M) return;
+    const int64_t rows = (int64_t)p.n_batch * p.Lq * p.M;
+    const int64_t row = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) / G;
+    const int g = threadIdx.x % G;
+    const bool live = row < rows;
     const int K = p.K;
+    const int64_t r0 = row * K;
     float dot = 0.f;
-    for (int k = 0; k < K; ++k) dot += attn[i * K + k] * grad_attn[i * K + k];
-    for (int k = 0; k < K; ++k) {
+    for (int k = g; k < K; k += G)
+        if (live) dot += attn[r0 + k] * grad_attn[r0 + k];
+    dot = group_sum<G>(dot);
+    if (!live) return;
+    for (int k = g; k < K; k += G) {
         const int l = k / p.P;
-        const int64_t s = i * K + k;
-        grad_logits[s] = attn[s] * (grad_attn[s] - dot);
-        const float2 g = reinterpret_cast<const float2*>(grad_loc)[s];
-        reinterpret_cast<float2*>(grad_offsets)[s] =
-            make_float2(g.x / (float)s_lvl[kMaxLevels + l], g.y / (float)s_lvl[l]);
+        grad_logits[r0 + k] = attn[r0 + k] * (grad_attn[r0 + k] - dot);
+        const float2 gl = reinterpret_cast<const float2*>(grad_loc)[r0 + k];
+        reinterpret_cast<float2*>(grad_offsets)[r0 + k] =
+            make_float2(gl.x / (float)s_lvl[kMaxLevels + l], gl.y / (float)s_lvl[l]);
     }
 }
+
+// Lanes per row: K rounded up to a power of two, at most 64.
+int lanes_per_row(int K) {
+    int g = 1;
+    while (g < K && g < 64) g <<= 1;
+    return g;
+}
+
+template <template <int> class Kern, typename... Args>
+hipError_t launch_rows(const Params& p, hipStream_t stream, Args... args) {
+    const int G = lanes_per_row(p.K);
+    const int64_t threads = (int64_t)p.n_batch * p.Lq * p.M * G;
+    const dim3 grid((unsigned)((threads + 255) / 256)), block(256);
+    switch (G) {
+        case 1: hipLaunchKernelGGL(Kern<1>::fn(), grid, block, 0, stream, p, args...); break;
+        case 2: hipLaunchKernelGGL(Kern<2>::fn(), grid, block, 0, stream, p, args...); break;
+        case 4: hipLaunchKernelGGL(Kern<4>::fn(), grid, block, 0, stream, p, args...); break;
+        case 8: hipLaunchKernelGGL(Kern<8>::fn(), grid, block, 0, stream, p, args...); break;
+        case 16: hipLaunchKernelGGL(Kern<16>::fn(), grid, block, 0, stream, p, args...); break;
+        case 32: hipLaunchKernelGGL(Kern<32>::fn(), grid, block, 0, stream, p, args...); break;
+        default: hipLaunchKernelGGL(Kern<64>::fn(), grid, block, 0, stream, p, args...); break;
+    }
+    return hipGetLastError();
+}
+
+template <int G>
+struct PrologueK {
+    static auto fn() { return prologue_kernel<G>; }
+};
+template <int G>
+struct PrologueGradK {
+    static auto fn() { return prologue_grad_kernel<G>; }
+};
 
 // One thread per (n, q, l): grad_ref summed over heads and points, in a fixed order.
 __global__ __launch_bounds__(256) void ref_grad_kernel(Params p, const float* grad_loc, float* grad_ref) {
@@ -72,19 +122,14 @@ __global__ __launch_bounds__(256) void ref_grad_kernel(Params p, const float* gr
 }  // namespace
 
 hipError_t launch_prologue(const Params& p, float* loc, float* attn, hipStream_t stream) {
-    const int64_t n = (int64_t)p.n_batch * p.Lq * p.M;
-    if (n == 0) return hipSuccess;
-    hipLaunchKernelGGL(prologue_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, stream, p, loc, attn);
-    return hipGetLastError();
+    if ((int64_t)p.n_batch * p.Lq * p.M == 0) return hipSuccess;
+    return launch_rows<PrologueK>(p, stream, loc, attn);
 }
 
 hipError_t launch_prologue_grad(const Params& p, const float* attn, const float* grad_loc, const float* grad_attn,
                                 float* grad_offsets, float* grad_logits, float* grad_ref, hipStream_t stream) {
-    const int64_t n = (int64_t)p.n_batch * p.Lq * p.M;
-    if (n == 0) return hipSuccess;
-    hipLaunchKernelGGL(prologue_grad_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, stream, p, attn,
-                       grad_loc, grad_attn, grad_offsets, grad_logits);
-    hipError_t e = hipGetLastError();
+    if ((int64_t)p.n_batch * p.Lq * p.M == 0) return hipSuccess;
+    hipError_t e = launch_rows<PrologueGradK>(p, stream, attn, grad_loc, grad_attn, grad_offsets, grad_logits);
     if (e != hipSuccess || !grad_ref) return e;
     const int64_t r = (int64_t)p.n_batch * p.Lq * p.L;
     hipLaunchKernelGGL(ref_grad_kernel, dim3((unsigned)((r + 255) / 256)), dim3(256), 0, stream, p, grad_loc,
