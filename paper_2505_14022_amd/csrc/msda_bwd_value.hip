@@ -598,11 +598,13 @@ __device__ __forceinline__ void flush_run(float4* acc, int key, int TH, int TW, 
 //   2. a scan over the keys gives each key's run start, and the records are placed in key order;
 //   3. the sorted records are cut into 64/kLPR equal slices, one per stream of kLPR lanes that
 //      share a record (32/kLPR channels per lane). A stream reads each record's grad_out row once
-//      and keeps the current run's four corner sums in registers; when the key changes the run is
-//      added into an LDS tile. A run that ends inside a slice ends in no other slice, so two
-//      streams never add the same key at once. The run a slice ends on may go on in the next
-//      slices: those last runs are added after the slices are done, one link of each chain of
-//      equal keys per round. (Fewer lanes per record spread the per-record work and the run ends
+//      and keeps the current run's four corner sums in registers; when the key changes the run
+//      moves to a second register set, and when a stream finishes a run while that set is full,
+//      every stream adds its waiting run into an LDS tile (one pass over the corners for all of
+//      them: 7 streams per pass at the DETR-encoder shape). A run that ends inside a slice ends in
+//      no other slice, so two streams never add the same key at once. The run a slice ends on may
+//      go on in the next slices: those last runs are added after the slices are done, one link of
+//      each chain of equal keys per round. (Fewer lanes per record spread the per-record work and the run ends
 //      over more streams: 4 lanes took 5 % off the backward against 8.)
 //   4. the tile's on-map pixels are stored once (plain stores), or added with atomics when the
 //      tile is split over several work items (its rows were zeroed before).
@@ -756,8 +758,8 @@ __global__ __launch_bounds__(256, 2) void fold_runs_kernel(Params p) {
             const int ch = ch0 + 4 * kQPL * sub;  // the lane's first channel
             for (int e = lane; e < kRunPix * kPixQ; e += 64) acc[e] = make_float4(0.f, 0.f, 0.f, 0.f);
             wave_lds_sync();
-            int cur = key_lo;
-            Corners run = {};
+            int cur = key_lo, pkey = -1;  // pkey: key of the finished run waiting in `pend`, or -1
+            Corners run = {}, pend = {};
             for (int b = 0; b < span; b += kRunBatch) {
                 uint32_t off[kRunBatch];
                 float ra[kRunBatch], rh[kRunBatch], rw[kRunBatch];
@@ -780,14 +782,23 @@ __global__ __launch_bounds__(256, 2) void fold_runs_kernel(Params p) {
 #pragma unroll
                 for (int u = 0; u < kRunBatch; ++u) {
                     const int pos = lo + b + u;
+                    const float h0f = floorf(rh[u]), w0f = floorf(rw[u]);
+                    const int key = key_of(h0f, w0f);
+                    const bool ends = pos < hi && key != cur;  // the run of key `cur` ends here
+                    // A finished run waits in `pend` until some stream finishes another one while
+                    // its own slot is full; then every waiting run is added at once, so one pass
+                    // over the corners serves many streams instead of one.
+                    if (__ballot(ends && pkey >= 0) != 0) {
+                        if (pkey >= 0) flush_run(acc, pkey, TH, TW, sub, pend);
+                        pkey = -1;
+                    }
+                    if (ends) {
+                        pend = run;
+                        pkey = cur;
+                        run = Corners{};
+                        cur = key;
+                    }
                     if (pos < hi) {
-                        const float h0f = floorf(rh[u]), w0f = floorf(rw[u]);
-                        const int key = key_of(h0f, w0f);
-                        if (key != cur) {  // the run of key `cur` ends before this record
-                            flush_run(acc, cur, TH, TW, sub, run);
-                            run = Corners{};
-                            cur = key;
-                        }
                         const float lh = rh[u] - h0f, lw = rw[u] - w0f, hh = 1.f - lh, hw = 1.f - lw, a = ra[u];
                         const float wk[4] = {a * (hh * hw), a * (hh * lw), a * (lh * hw), a * (lh * lw)};
 #pragma unroll
@@ -797,6 +808,8 @@ __global__ __launch_bounds__(256, 2) void fold_runs_kernel(Params p) {
                     }
                 }
             }
+            // the finished runs still waiting (their keys differ: each ended inside its own slice)
+            if (pkey >= 0) flush_run(acc, pkey, TH, TW, sub, pend);
             // the runs the slices end on: a key may end several neighbouring slices. Each slice
             // counts the earlier slices that end on its key; round j adds the sums of the slices
             // with count j, so no two streams add the same key at once
