@@ -29,11 +29,16 @@
  *   grad_attn    [N, Lq, M, L, P]    fp32
  *
  * Ownership and execution. All tensor pointers are DEVICE pointers owned by the caller, except the
- * two level tables, which are HOST pointers read during the call. The library allocates no memory
- * (the backward's scratch is a caller-provided workspace), keeps no state between calls, never
- * synchronizes and never prints. Work is enqueued on `stream` (a hipStream_t; NULL means the
- * default stream) and the call returns before it completes. Outputs are overwritten entirely and
- * must not alias inputs or the workspace. Inputs are not modified.
+ * two level tables, which are HOST pointers read during the call. The library allocates no device
+ * memory (the backward's scratch is a caller-provided workspace), never synchronizes and never
+ * prints. Work is enqueued on `stream` (a hipStream_t; NULL means the default stream) and the call
+ * returns before it completes. The owner-computes backward runs its grad_value kernels on a second
+ * stream, forked from `stream` at the start of the call and joined back into it before the call's
+ * last work item, so everything enqueued on `stream` afterwards is ordered after all of the call's
+ * work (also under stream capture). That stream and its two events are the only state the library
+ * keeps: one set per (host thread, device), created by the first such call and kept for the life of
+ * the thread; if they cannot be created the call runs on `stream` alone. Outputs are overwritten
+ * entirely and must not alias inputs or the workspace. Inputs are not modified.
  * Arithmetic is fp32 (fp16 inputs are converted exactly; fp16 out is rounded to nearest-even
  * once). The order in which contributions to one grad_value element are summed depends on
  * scheduling, so its low bits may differ between runs; out, grad_loc and grad_attn are

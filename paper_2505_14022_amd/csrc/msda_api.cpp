@@ -128,6 +128,40 @@ size_t fused_staging_bytes(int64_t N, int64_t S, int64_t M, int64_t D, int64_t L
     return 2 * round_up(per * 8) + 2 * round_up(per * 4);
 }
 
+// A second stream for the backward: the grad_value pipeline (binning and fold) and the
+// grad_loc / grad_attn kernel read the same inputs and write disjoint outputs, so they run side by
+// side, forked from and joined back into the caller's stream with two events. One stream and two
+// events per (host thread, device), created on first use and kept for the life of the thread; if
+// they cannot be created the backward runs on the caller's stream alone.
+struct SideStream {
+    hipStream_t s = nullptr;
+    hipEvent_t fork = nullptr, join = nullptr;
+    bool tried = false;
+};
+constexpr int kMaxDevices = 64;
+// The events order work between two streams of one device: a device-scope fence is enough.
+constexpr unsigned kSideEventFlags = hipEventDisableTiming | hipEventDisableSystemFence;
+
+SideStream* side_stream() {
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
+    thread_local SideStream table[kMaxDevices];
+    SideStream& x = table[dev];
+    if (!x.tried) {
+        x.tried = true;
+        if (hipStreamCreateWithFlags(&x.s, hipStreamNonBlocking) != hipSuccess) {
+            x.s = nullptr;
+        } else if (hipEventCreateWithFlags(&x.fork, kSideEventFlags) != hipSuccess ||
+                   hipEventCreateWithFlags(&x.join, kSideEventFlags) != hipSuccess) {
+            if (x.fork) (void)hipEventDestroy(x.fork);
+            (void)hipStreamDestroy(x.s);
+            x.s = nullptr;
+        }
+        (void)hipGetLastError();  // a failed creation leaves nothing for the next call to report
+    }
+    return x.s ? &x : nullptr;
+}
+
 // Shared body of both backward entry points (arguments already checked, except value / grad_out /
 // grad_value). `pro` is null for the plain entry point; with it, each batch chunk first computes
 // its locations and weights into the staging buffers of `smp` and ends with the prologue's gradient.
@@ -175,16 +209,21 @@ msda_status_t backward_body(const void* value, const int64_t* shapes, const int6
             e = msda::launch_prologue(p, const_cast<float*>(p.loc), const_cast<float*>(p.attn), s);
             if (e != hipSuccess) return fail(MSDA_ERROR_LAUNCH_FAILED, "prologue launch: %s", hipGetErrorString(e));
         }
-        e = msda::launch_backward_grads(p, (msda_dtype_t)dtype, !binned, s);
-        if (e != hipSuccess) return fail(MSDA_ERROR_LAUNCH_FAILED, "backward launch: %s", hipGetErrorString(e));
+        // grad_value (binned) on the side stream, forked after everything enqueued on `s` so far
+        SideStream* side = binned ? side_stream() : nullptr;
+        if (side && ((e = hipEventRecord(side->fork, s)) != hipSuccess ||
+                     (e = hipStreamWaitEvent(side->s, side->fork, 0)) != hipSuccess))
+            return fail(MSDA_ERROR_LAUNCH_FAILED, "backward fork: %s", hipGetErrorString(e));
         if (binned) {
             if (!msda::plan_binned(p))
                 return fail(MSDA_ERROR_LAUNCH_FAILED, "internal: binned plan changed between batches");
             msda::bind_workspace(p, workspace);
-            e = msda::launch_backward_value_binned(p, (msda_dtype_t)dtype, s);
+            e = msda::launch_backward_value_binned(p, (msda_dtype_t)dtype, side ? side->s : s);
             if (e != hipSuccess)
                 return fail(MSDA_ERROR_LAUNCH_FAILED, "backward grad_value launch: %s", hipGetErrorString(e));
         }
+        e = msda::launch_backward_grads(p, (msda_dtype_t)dtype, !binned, s);
+        if (e != hipSuccess) return fail(MSDA_ERROR_LAUNCH_FAILED, "backward launch: %s", hipGetErrorString(e));
         if (pro) {
             const int64_t q0 = n0 * Lq * M * L * P;
             e = msda::launch_prologue_grad(p, p.attn, p.grad_loc, p.grad_attn, pro->grad_offsets + q0 * 2,
@@ -193,6 +232,10 @@ msda_status_t backward_body(const void* value, const int64_t* shapes, const int6
             if (e != hipSuccess)
                 return fail(MSDA_ERROR_LAUNCH_FAILED, "prologue gradient launch: %s", hipGetErrorString(e));
         }
+        // join before anything after this chunk (the next chunk reuses the staging and workspace)
+        if (side && ((e = hipEventRecord(side->join, side->s)) != hipSuccess ||
+                     (e = hipStreamWaitEvent(s, side->join, 0)) != hipSuccess))
+            return fail(MSDA_ERROR_LAUNCH_FAILED, "backward join: %s", hipGetErrorString(e));
     }
     return ok();
 }

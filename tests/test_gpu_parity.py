@@ -176,6 +176,75 @@ def test_side_stream():
     assert normwise(gv.cpu().numpy(), ref["grad_value"]) <= 1e-4
 
 
+def test_backward_on_two_user_streams():
+    # the owner-computes backward forks its grad_value work onto a library stream and joins it
+    # back; calls on two user streams from one thread must each see their own inputs
+    import torch
+
+    cases = [workloads.random_case(1, 4, 32, ((24, 20), (12, 10)), 4, 2000, "f32", seed=20 + i) for i in range(2)]
+    say("backward on two user streams")
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    dev = [to_device(c) for c in cases]
+    torch.cuda.synchronize()
+    res = []
+    for c, d, st in zip(cases, dev, streams):
+        with torch.cuda.stream(st):
+            res.append(msda.backward(d.value, c.shapes, c.starts, d.loc, d.attn, d.grad_out, workspace="owner",
+                                     stream=st))
+    torch.cuda.synchronize()
+    for c, r in zip(cases, res):
+        ref = run_oracle(c)
+        assert normwise(r[0].cpu().numpy(), ref["grad_value"]) <= 1e-4
+        assert normwise(r[1].cpu().numpy(), ref["grad_loc"]) <= 1e-3
+        assert normwise(r[2].cpu().numpy(), ref["grad_attn"]) <= 1e-3
+
+
+def test_backward_graph_replays():
+    # forward + backward captured into a graph (the grad_value fork and join included), replayed
+    # several times with eager work in between; every replay must match the eager results
+    import torch
+
+    inp = workloads.random_case(2, 4, 32, ((24, 20), (12, 10)), 4, 1500, "f32", seed=31)
+    d = to_device(inp)
+    say("graph capture and replays of forward + backward")
+    w = inp.w
+    ws = torch.empty(msda.workspace_size(inp.shapes, inp.starts, w.N, w.S, w.M, w.D, w.Lq, w.L, w.P, msda.MSDA_F32,
+                                         msda.MSDA_WORKSPACE_OWNER),
+                     dtype=torch.uint8, device="cuda")
+    out = torch.empty((2, 1500, 128), device="cuda")
+    gv = torch.empty(tuple(inp.value.shape), device="cuda")
+    gl = torch.empty(tuple(inp.loc.shape), device="cuda")
+    ga = torch.empty(tuple(inp.attn.shape), device="cuda")
+
+    def step(stream):
+        msda.forward(d.value, inp.shapes, inp.starts, d.loc, d.attn, out=out, stream=stream)
+        msda.backward(d.value, inp.shapes, inp.starts, d.loc, d.attn, d.grad_out, gv, gl, ga, workspace=ws,
+                      stream=stream)
+
+    step(torch.cuda.current_stream())
+    torch.cuda.synchronize()
+    eager = [x.cpu().numpy() for x in (out, gv, gl, ga)]
+    g = torch.cuda.CUDAGraph()
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        with torch.cuda.graph(g, stream=s):
+            step(s)
+    torch.cuda.synchronize()
+    for rep in range(3):
+        for x in (out, gv, gl, ga):
+            x.fill_(float("nan"))
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        got = [x.cpu().numpy() for x in (out, gv, gl, ga)]
+        assert np.array_equal(got[0], eager[0]), f"replay {rep}: out differs"
+        assert np.array_equal(got[2], eager[2]) and np.array_equal(got[3], eager[3]), f"replay {rep}: grad_loc/attn"
+        assert np.all(np.isfinite(got[1])) and normwise(got[1], eager[1]) < 1e-6, f"replay {rep}: grad_value"
+        step(torch.cuda.current_stream())  # eager work between the replays
+        torch.cuda.synchronize()
+
+
 def test_adjoint_identities_on_gpu_results():
     # out is linear in value and attn: <g, out> = <grad_value, value> = <grad_attn, attn>
     w = workloads.BY_NAME["detr_encoder"]
