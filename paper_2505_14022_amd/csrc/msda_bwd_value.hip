@@ -595,7 +595,10 @@ __device__ __forceinline__ void flush_run(float4* acc, int key, int TH, int TW, 
 // queue so that a grid of resident workgroups stays busy to the end:
 //   1. every lane loads kChunkRecords/64 records (all loads in flight together) and keys each by
 //      the tile position of its top-left corner; LDS counters rank the records per key;
-//   2. a scan over the keys gives each key's run start, and the records are placed in key order;
+//   2. a scan over the keys gives each key's run start, and the records are placed in key order,
+//      with their coordinates replaced by the fractional parts and their keys stored beside them,
+//      so the per-record work below needs neither floor nor key arithmetic. The next item's
+//      descriptor is loaded at this point, so it has arrived when the item is done;
 //   3. the sorted records are cut into 64/kLPR equal slices, one per stream of kLPR lanes that
 //      share a record (32/kLPR channels per lane). A stream reads each record's grad_out row once
 //      and keeps the current run's four corner sums in registers; when the key changes the run
@@ -613,28 +616,56 @@ template <typename T>
 __global__ __launch_bounds__(256, 2) void fold_runs_kernel(Params p) {
     __shared__ int s_geo[kGeo * kMaxLevels];
     __shared__ int s_start[kAccWaves][kRunKeys + 1];
-    __shared__ int4 s_rec[kAccWaves][kChunkRecords];        // records sorted by key
+    __shared__ int4 s_rec[kAccWaves][kChunkRecords];        // sorted records: {grad_out row, a, lh, lw}
+    __shared__ int s_key[kAccWaves][kChunkRecords];         // and their keys
     __shared__ float4 s_acc[kAccWaves][kRunPix * kPixQ];    // 32 channels of the tile
     load_geo(p, s_geo);
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
     int* start = s_start[wave];
     int4* srec = s_rec[wave];
+    int* skey = s_key[wave];
     float4* acc = s_acc[wave];
     const int D = p.D;
     const rsrc_t gr = make_rsrc(p.grad_out, (uint32_t)((size_t)p.n_batch * p.Lq * p.M * D * sizeof(T)));
     const int sub = lane % kLPR, grp = lane / kLPR;  // lane within its record stream, stream
+    constexpr int kRecPerLane = kChunkRecords / 64;
 
     // Work items are dealt from eight queues: queue x holds items x, x + 8, x + 16, ... and serves
     // the waves of XCD x (workgroups are dispatched to the eight XCDs in turn). The waves in flight
     // still work on neighbouring items in slab-major order. Each counter has a 256-byte line of its
     // own: all waves taking items from one counter (or from counters sharing a line) serialize on
     // it, which cost the fold a quarter of its time. A wave whose queue has drained helps the others.
-    const int total = p.tile_chunks[p.n_tiles];
+    int total = p.tile_chunks[p.n_tiles];
+    total = total < 0 ? 0 : (total > p.max_items ? p.max_items : total);
     int owner = blockIdx.x & (kQueues - 1), visited = 0;
     auto owned = [&](int q) { return (total - q + kQueues - 1) / kQueues; };
     auto counter = [&](int q) { return p.queue + q * kQueueStride; };
+    // descriptor of work item `it`: lanes 0..15 hold its 16 words
+    auto load_desc = [&](int it) { return lane < 16 ? p.item_desc[(size_t)it * 16 + lane] : 0; };
+    // the item's visible records, kRecPerLane per lane (all loads in flight together); rows past
+    // the item's end are marked with x = -1
+    auto load_records = [&](int dv, int4 (&rc)[kRecPerLane]) {
+        const int beg = __builtin_amdgcn_readlane(dv, 0), end = __builtin_amdgcn_readlane(dv, 1);
+        const int a0 = __builtin_amdgcn_readlane(dv, 8), na = __builtin_amdgcn_readlane(dv, 9);
+        const int b0 = __builtin_amdgcn_readlane(dv, 10), nb = __builtin_amdgcn_readlane(dv, 11);
+        const int c0 = __builtin_amdgcn_readlane(dv, 12), nc = __builtin_amdgcn_readlane(dv, 13);
+        const int d0 = __builtin_amdgcn_readlane(dv, 14);
+        const int4* records = reinterpret_cast<const int4*>(p.records);
+#pragma unroll
+        for (int i = 0; i < kRecPerLane; ++i) {
+            int pos = beg + i * 64 + lane, idx = -1;
+            if (pos < end) {
+                if (pos < na) idx = a0 + pos;
+                else if ((pos -= na) < nb) idx = b0 + pos;
+                else if ((pos -= nb) < nc) idx = c0 + pos;
+                else idx = d0 + (pos - nc);
+            }
+            rc[i] = idx >= 0 && idx < p.n_samples ? records[idx] : make_int4(-1, 0, 0, 0);
+        }
+    };
     int taken = 0;
     if (lane == 0) taken = atomicAdd(counter(owner), 1);
+    int pf_item = -1, pf_dv = 0;  // the next item of this queue and its prefetched descriptor
     for (;;) {
         const int slot = __builtin_amdgcn_readfirstlane(taken);
         if (slot >= owned(owner)) {  // this queue has drained: go to the next one
@@ -652,20 +683,18 @@ __global__ __launch_bounds__(256, 2) void fold_runs_kernel(Params p) {
         const int item = slot * kQueues + owner;
         // the next slot is taken now; it is needed only when this item is done
         if (lane == 0) taken = atomicAdd(counter(owner), 1);
-        int dv = 0;
-        if (lane < 16) dv = p.item_desc[(size_t)item * 16 + lane];
-        const int beg = __builtin_amdgcn_readlane(dv, 0), end = __builtin_amdgcn_readlane(dv, 1);
+        const int dv = item == pf_item ? pf_dv : load_desc(item);
+        int4 rc[kRecPerLane];
+        load_records(dv, rc);
         const bool split = __builtin_amdgcn_readlane(dv, 2) != 0;
         const int l = __builtin_amdgcn_readlane(dv, 3);
         const int n = __builtin_amdgcn_readlane(dv, 4), m = __builtin_amdgcn_readlane(dv, 5);
         const int h_org = __builtin_amdgcn_readlane(dv, 6), w_org = __builtin_amdgcn_readlane(dv, 7);
-        const int a0 = __builtin_amdgcn_readlane(dv, 8), na = __builtin_amdgcn_readlane(dv, 9);
-        const int b0 = __builtin_amdgcn_readlane(dv, 10), nb = __builtin_amdgcn_readlane(dv, 11);
-        const int c0 = __builtin_amdgcn_readlane(dv, 12), nc = __builtin_amdgcn_readlane(dv, 13);
-        const int d0 = __builtin_amdgcn_readlane(dv, 14);
-        if (l < 0 || l >= p.L) continue;  // never taken: descriptors name a level of the map
+        // never taken: descriptors name a tile of the map
+        if (l < 0 || l >= p.L || n < 0 || n >= p.n_batch || m < 0 || m >= p.M) continue;
         const int H = __builtin_amdgcn_readfirstlane(s_geo[l]);
         const int W = __builtin_amdgcn_readfirstlane(s_geo[kMaxLevels + l]);
+        if (h_org < 0 || h_org >= H || w_org < 0 || w_org >= W) continue;
         const int th = __builtin_amdgcn_readfirstlane(s_geo[2 * kMaxLevels + l]);
         const int tw = __builtin_amdgcn_readfirstlane(s_geo[3 * kMaxLevels + l]);
         const int TH = 1 << th, TW = 1 << tw;
@@ -673,23 +702,8 @@ __global__ __launch_bounds__(256, 2) void fold_runs_kernel(Params p) {
         const int th_on = min(TH, H - h_org), tw_on = min(TW, W - w_org);  // tile pixels on the map
         const int nkeys = (TH + 1) << kKeyShift;
 
-        // 1. load the records and rank them per key
-        constexpr int kRecPerLane = kChunkRecords / 64;
-        int4 rc[kRecPerLane];
-        {
-            const int4* records = reinterpret_cast<const int4*>(p.records);
-#pragma unroll
-            for (int i = 0; i < kRecPerLane; ++i) {
-                int pos = beg + i * 64 + lane, idx = -1;
-                if (pos < end) {
-                    if (pos < na) idx = a0 + pos;
-                    else if ((pos -= na) < nb) idx = b0 + pos;
-                    else if ((pos -= nb) < nc) idx = c0 + pos;
-                    else idx = d0 + (pos - nc);
-                }
-                rc[i] = idx >= 0 && idx < p.n_samples ? records[idx] : make_int4(-1, 0, 0, 0);
-            }
-        }
+        // 1. rank the records per key (the key of a record: the tile position of its top-left
+        //    corner), and replace its coordinates by their fractional parts
         wave_lds_sync();  // the previous item is done with this wave's LDS
         for (int k = lane; k <= kRunKeys; k += 64) start[k] = 0;
         wave_lds_sync();
@@ -699,11 +713,14 @@ __global__ __launch_bounds__(256, 2) void fold_runs_kernel(Params p) {
             key[i] = -1;
             rank[i] = 0;
             if (rc[i].x >= 0) {
-                const int r = (int)floorf(__builtin_bit_cast(float, rc[i].z)) - h_org;
-                const int c = (int)floorf(__builtin_bit_cast(float, rc[i].w)) - w_org;
+                const float hf = floorf(__builtin_bit_cast(float, rc[i].z));
+                const float wf = floorf(__builtin_bit_cast(float, rc[i].w));
+                const int r = (int)hf - h_org, c = (int)wf - w_org;
                 if (r >= -1 && r < TH && c >= -1 && c < TW) {  // always true for a visible record
                     key[i] = ((r + 1) << kKeyShift) + c + 1;
                     rank[i] = atomicAdd(&start[key[i]], 1);
+                    rc[i].z = __builtin_bit_cast(int, __builtin_bit_cast(float, rc[i].z) - hf);
+                    rc[i].w = __builtin_bit_cast(int, __builtin_bit_cast(float, rc[i].w) - wf);
                 }
             }
         }
@@ -737,37 +754,46 @@ __global__ __launch_bounds__(256, 2) void fold_runs_kernel(Params p) {
         for (int i = 0; i < kRecPerLane; ++i) {
             if (key[i] >= 0) {
                 const int at = start[key[i]] + rank[i];
-                if (at < kChunkRecords) srec[at] = rc[i];
+                if (at < kChunkRecords) {
+                    srec[at] = rc[i];
+                    skey[at] = key[i];
+                }
             }
         }
         wave_lds_sync();
+
+        // the next item of this queue: its descriptor is loaded now, while this item is folded
+        pf_item = -1;
+        {
+            const int nslot = __builtin_amdgcn_readfirstlane(taken);
+            if (nslot < owned(owner)) {
+                pf_item = nslot * kQueues + owner;
+                pf_dv = load_desc(pf_item);
+            }
+        }
 
         // 3. slices of equal length
         const int C = start[nkeys];
         const int lo = (C * grp) / kGroups, hi = (C * (grp + 1)) / kGroups;
         const int span = (C + kGroups - 1) / kGroups;
-        auto key_of = [&](float h0f, float w0f) {
-            return (((int)h0f - h_org + 1) << kKeyShift) + ((int)w0f - w_org + 1);
-        };
-        int key_lo = 0;  // key of the slice's first record
-        if (hi > lo) {
-            const int4 e = srec[lo];
-            key_lo = key_of(floorf(__builtin_bit_cast(float, e.z)), floorf(__builtin_bit_cast(float, e.w)));
-        }
+        const int key_lo = hi > lo ? skey[lo] : 0;  // key of the slice's first record
         for (int ch0 = 0; ch0 < D; ch0 += 4 * kPixQ) {
             const int ch = ch0 + 4 * kQPL * sub;  // the lane's first channel
-            for (int e = lane; e < kRunPix * kPixQ; e += 64) acc[e] = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+            for (int it = 0; it < kRunPix * kPixQ / 64; ++it) acc[lane + 64 * it] = make_float4(0.f, 0.f, 0.f, 0.f);
             wave_lds_sync();
             int cur = key_lo, pkey = -1;  // pkey: key of the finished run waiting in `pend`, or -1
             Corners run = {}, pend = {};
             for (int b = 0; b < span; b += kRunBatch) {
                 uint32_t off[kRunBatch];
                 float ra[kRunBatch], rh[kRunBatch], rw[kRunBatch];
+                int rk[kRunBatch];
 #pragma unroll
                 for (int u = 0; u < kRunBatch; ++u) {
                     const int pos = lo + b + u;
                     const bool act = pos < hi;
                     const int4 e = srec[act ? pos : 0];
+                    rk[u] = skey[act ? pos : 0];
                     off[u] = act ? (uint32_t)(e.x + ch) : (uint32_t)kOOBElem;
                     ra[u] = act ? __builtin_bit_cast(float, e.y) : 0.f;
                     rh[u] = __builtin_bit_cast(float, e.z);
@@ -782,8 +808,7 @@ __global__ __launch_bounds__(256, 2) void fold_runs_kernel(Params p) {
 #pragma unroll
                 for (int u = 0; u < kRunBatch; ++u) {
                     const int pos = lo + b + u;
-                    const float h0f = floorf(rh[u]), w0f = floorf(rw[u]);
-                    const int key = key_of(h0f, w0f);
+                    const int key = rk[u];
                     const bool ends = pos < hi && key != cur;  // the run of key `cur` ends here
                     // A finished run waits in `pend` until some stream finishes another one while
                     // its own slot is full; then every waiting run is added at once, so one pass
@@ -799,8 +824,9 @@ __global__ __launch_bounds__(256, 2) void fold_runs_kernel(Params p) {
                         cur = key;
                     }
                     if (pos < hi) {
-                        const float lh = rh[u] - h0f, lw = rw[u] - w0f, hh = 1.f - lh, hw = 1.f - lw, a = ra[u];
-                        const float wk[4] = {a * (hh * hw), a * (hh * lw), a * (lh * hw), a * (lh * lw)};
+                        const float lh = rh[u], lw = rw[u], a = ra[u];
+                        const float ah = a * (1.f - lh), al = a * lh, hw = 1.f - lw;
+                        const float wk[4] = {ah * hw, ah * lw, al * hw, al * lw};
 #pragma unroll
                         for (int k = 0; k < 4; ++k)
 #pragma unroll
@@ -826,25 +852,31 @@ __global__ __launch_bounds__(256, 2) void fold_runs_kernel(Params p) {
             wave_lds_sync();
             // 4. store the tile's on-map pixels
             if (!split) {
-                for (int e = lane; e < kRunPix * kPixQ; e += 64) {
+#pragma unroll 4
+                for (int it = 0; it < kRunPix * kPixQ / 64; ++it) {
+                    const int e = lane + 64 * it;
                     const int px = e / kPixQ, q = e - px * kPixQ;
                     const int r = px >> tw, c = px & (TW - 1);
+                    const float4 v = acc[e];
                     if (px < TH * TW && r < th_on && c < tw_on && ch0 + 4 * q < D) {
                         float* dst = p.grad_value + ((size_t)(n * p.S + st + (h_org + r) * W + w_org + c) * p.M + m) * D +
                                      ch0 + 4 * q;
-                        *reinterpret_cast<float4*>(dst) = acc[e];
+                        *reinterpret_cast<float4*>(dst) = v;
                     }
                 }
             } else {
                 // one channel per lane: the atomics of a wave cover whole rows
                 const float* accf = reinterpret_cast<const float*>(acc);
-                for (int e = lane; e < kRunPix * 4 * kPixQ; e += 64) {
+#pragma unroll 8
+                for (int it = 0; it < kRunPix * 4 * kPixQ / 64; ++it) {
+                    const int e = lane + 64 * it;
                     const int px = e / (4 * kPixQ), cc = e - px * (4 * kPixQ);
                     const int r = px >> tw, c = px & (TW - 1);
+                    const float v = accf[e];
                     if (px < TH * TW && r < th_on && c < tw_on && ch0 + cc < D) {
                         float* dst = p.grad_value + ((size_t)(n * p.S + st + (h_org + r) * W + w_org + c) * p.M + m) * D +
                                      ch0 + cc;
-                        unsafeAtomicAdd(dst, accf[e]);
+                        unsafeAtomicAdd(dst, v);
                     }
                 }
             }
