@@ -209,15 +209,20 @@ msda_status_t backward_body(const void* value, const int64_t* shapes, const int6
             e = msda::launch_prologue(p, const_cast<float*>(p.loc), const_cast<float*>(p.attn), s);
             if (e != hipSuccess) return fail(MSDA_ERROR_LAUNCH_FAILED, "prologue launch: %s", hipGetErrorString(e));
         }
+        if (binned) {
+            if (!msda::plan_binned(p))
+                return fail(MSDA_ERROR_LAUNCH_FAILED, "internal: binned plan changed between batches");
+            msda::bind_workspace(p, workspace);
+            // the workspace's counters are zeroed on `s`, before the grid-wide work starts there
+            if ((e = msda::launch_binned_reset(p, s)) != hipSuccess)
+                return fail(MSDA_ERROR_LAUNCH_FAILED, "workspace reset: %s", hipGetErrorString(e));
+        }
         // grad_value (binned) on the side stream, forked after everything enqueued on `s` so far
         SideStream* side = binned ? side_stream() : nullptr;
         if (side && ((e = hipEventRecord(side->fork, s)) != hipSuccess ||
                      (e = hipStreamWaitEvent(side->s, side->fork, 0)) != hipSuccess))
             return fail(MSDA_ERROR_LAUNCH_FAILED, "backward fork: %s", hipGetErrorString(e));
         if (binned) {
-            if (!msda::plan_binned(p))
-                return fail(MSDA_ERROR_LAUNCH_FAILED, "internal: binned plan changed between batches");
-            msda::bind_workspace(p, workspace);
             e = msda::launch_backward_value_binned(p, (msda_dtype_t)dtype, side ? side->s : s);
             if (e != hipSuccess)
                 return fail(MSDA_ERROR_LAUNCH_FAILED, "backward grad_value launch: %s", hipGetErrorString(e));

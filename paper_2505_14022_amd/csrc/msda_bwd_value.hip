@@ -10,9 +10,12 @@
 //               tiles its other corners reach (class: interior / right / right+down / down).
 //               Workgroups count in an LDS histogram and add their totals to the global counts.
 //   2. scan:    exclusive prefix sums over bins (record offsets) and over tiles (work items: a
-//               tile whose visible samples exceed one chunk is split into several items).
-//   3. scatter: each sample's index is written into its bin (LDS ranks + one global atomic per
-//               workgroup and bin).
+//               tile whose visible samples exceed one chunk is split into several items), in two
+//               launches: per-workgroup totals (the last workgroup to finish scans the totals),
+//               then the per-tile offsets.
+//   3. scatter: each sample's record is written into its bin (LDS ranks + one global atomic per
+//               workgroup and bin); the same launch writes the fold's work-item descriptors and
+//               zeroes the grad_value rows of tiles that several work items add into.
 //   4. fold:    one wave per work item zeroes an LDS tile, folds a*w_corner*g of every visible
 //               sample (own bin plus the left / up / up-left neighbours' straddling classes)
 //               and stores the tile's grad_value rows; items of a split tile add theirs with
@@ -171,6 +174,24 @@ __device__ __forceinline__ int2 block_scan2(int a, int b, int& pa, int& pb, int*
 
 constexpr int kTilesPerThread = kScanTiles / 256;
 
+// Exclusive scan of the per-block totals, in place, by one workgroup.
+__device__ __forceinline__ void scan_block_sums(const Params& p, int* s) {
+    int carry_a = 0, carry_b = 0;
+    for (int base = 0; base < p.scan_blocks; base += 256) {
+        const int i = base + threadIdx.x;
+        const int a = i < p.scan_blocks ? p.block_sums[2 * i] : 0;
+        const int b = i < p.scan_blocks ? p.block_sums[2 * i + 1] : 0;
+        int pa, pb;
+        const int2 tot = block_scan2(a, b, pa, pb, s);
+        if (i < p.scan_blocks) {
+            p.block_sums[2 * i] = carry_a + pa;
+            p.block_sums[2 * i + 1] = carry_b + pb;
+        }
+        carry_a += tot.x;
+        carry_b += tot.y;
+    }
+}
+
 __global__ __launch_bounds__(256) void scan_reduce_kernel(Params p) {
     __shared__ int s_geo[kGeo * kMaxLevels];
     __shared__ int s[512];
@@ -187,29 +208,20 @@ __global__ __launch_bounds__(256) void scan_reduce_kernel(Params p) {
     }
     int pa, pb;
     const int2 tot = block_scan2(own_sum, item_sum, pa, pb, s);
+    // The last workgroup to finish turns the per-block totals into exclusive prefixes: each
+    // workgroup publishes its totals (release) before counting itself done, and the last one
+    // reads them after its count (acquire).
+    __shared__ int s_last;
     if (threadIdx.x == 0) {
         p.block_sums[2 * blockIdx.x] = tot.x;
         p.block_sums[2 * blockIdx.x + 1] = tot.y;
+        const int done = __hip_atomic_fetch_add(p.scan_done, 1, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
+        s_last = done == p.scan_blocks - 1;
     }
-}
-
-// One workgroup: exclusive scan of the per-block totals, in place.
-__global__ __launch_bounds__(256) void scan_blocks_kernel(Params p) {
-    __shared__ int s[512];
-    int carry_a = 0, carry_b = 0;
-    for (int base = 0; base < p.scan_blocks; base += 256) {
-        const int i = base + threadIdx.x;
-        const int a = i < p.scan_blocks ? p.block_sums[2 * i] : 0;
-        const int b = i < p.scan_blocks ? p.block_sums[2 * i + 1] : 0;
-        int pa, pb;
-        const int2 tot = block_scan2(a, b, pa, pb, s);
-        if (i < p.scan_blocks) {
-            p.block_sums[2 * i] = carry_a + pa;
-            p.block_sums[2 * i + 1] = carry_b + pb;
-        }
-        carry_a += tot.x;
-        carry_b += tot.y;
-    }
+    __syncthreads();
+    if (!s_last) return;
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+    scan_block_sums(p, s);
 }
 
 __global__ __launch_bounds__(256) void scan_apply_kernel(Params p) {
@@ -253,12 +265,7 @@ __global__ __launch_bounds__(256) void scan_apply_kernel(Params p) {
 //   descriptor: {beg, end, split, level, n, m, h_org, w_org, own start, own count, left start,
 //                left count, up start, up count, up-left start, 0}: the item folds visible records
 //                [beg, end) of the tile, counted through the own / left / up / up-left bin ranges
-__global__ __launch_bounds__(256) void prep_items_kernel(Params p) {
-    __shared__ int s_geo[kGeo * kMaxLevels];
-    load_geo(p, s_geo);
-    const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
-    const int lane = threadIdx.x & 63;
-    if (t >= p.n_tiles) return;
+__device__ __forceinline__ void prep_tile(const Params& p, const int* s_geo, int t, int lane) {
     const int first = p.tile_chunks[t];
     const int nit = p.tile_chunks[t + 1] - first;
     const int slab = t / p.tiles_per_slab, tin = t - slab * p.tiles_per_slab;
@@ -297,12 +304,9 @@ __global__ __launch_bounds__(256) void prep_items_kernel(Params p) {
 
 constexpr int kScatterRounds = kCountQueries / 256;
 
-__global__ __launch_bounds__(256) void bin_scatter_kernel(Params p) {
-    extern __shared__ int hist[];  // bins of this slab
-    __shared__ int s_geo[kGeo * kMaxLevels];
-    const int bps = p.tiles_per_slab * 4;
-    for (int i = threadIdx.x; i < bps; i += 256) hist[i] = 0;
-    load_geo(p, s_geo);
+// Records of one workgroup's (slab, chunk of queries): ranks within the workgroup from LDS
+// counters, one global atomic per bin for the workgroup's base, then the record stores.
+__device__ __forceinline__ void scatter_chunk(const Params& p, const int* s_geo, int* hist, int bps) {
     const int slab = blockIdx.x / p.chunks, chunk = blockIdx.x - slab * p.chunks;
     const int n = slab / p.M, m = slab - n * p.M;
     const int q0 = chunk * p.q_per_block;
@@ -345,6 +349,19 @@ __global__ __launch_bounds__(256) void bin_scatter_kernel(Params p) {
         const int pos = hist[bins[r]] + ranks[r];
         if (pos < p.n_samples) records[pos] = rec[r];  // always true when counts and cursor agree
     }
+}
+
+// Workgroups past n_slabs * chunks only prepare work items (below).
+__global__ __launch_bounds__(256) void bin_scatter_kernel(Params p) {
+    extern __shared__ int hist[];  // bins of this slab
+    __shared__ int s_geo[kGeo * kMaxLevels];
+    const int bps = p.tiles_per_slab * 4;
+    for (int i = threadIdx.x; i < bps; i += 256) hist[i] = 0;
+    load_geo(p, s_geo);
+    if (blockIdx.x < p.n_slabs * p.chunks) scatter_chunk(p, s_geo, hist, bps);
+    // descriptors of the fold's work items (and zeroed rows of split tiles), a few tiles per wave
+    for (int t = blockIdx.x * 4 + (threadIdx.x >> 6); t < p.n_tiles; t += gridDim.x * 4)
+        prep_tile(p, s_geo, t, threadIdx.x & 63);
 }
 
 // ---------------------------------------------------------------- 4. fold
@@ -999,9 +1016,13 @@ int queue_grid() {
 }
 }  // namespace
 
+// Ints of the workspace's zeroed head: the per-bin counts, the fold's queue counters and the scan's
+// count of finished workgroups, each counter on a 256-byte line of its own.
+size_t zeroed_ints(const Params& p) { return (size_t)p.n_tiles * 4 + (kQueues + 1) * kQueueStride; }
+
 size_t binned_workspace_bytes(const Params& p) {
     const size_t nb = (size_t)p.n_tiles * 4;
-    return align256((nb + kQueues * kQueueStride) * 4) + align256((size_t)p.max_items * 64) + align256((nb + 1) * 4) + align256(nb * 4) +
+    return align256(zeroed_ints(p) * 4) + align256((size_t)p.max_items * 64) + align256((nb + 1) * 4) + align256(nb * 4) +
            align256(((size_t)p.n_tiles + 1) * 4) +
            align256((size_t)p.max_items * 4) + align256((size_t)p.scan_blocks * 2 * 4) +
            align256((size_t)p.n_samples * 16);
@@ -1012,7 +1033,8 @@ void bind_workspace(Params& p, void* ws) {
     const size_t nb = (size_t)p.n_tiles * 4;
     p.counts = reinterpret_cast<int*>(c);
     p.queue = p.counts + nb;
-    c += align256((nb + kQueues * kQueueStride) * 4);
+    p.scan_done = p.queue + kQueues * kQueueStride;
+    c += align256(zeroed_ints(p) * 4);
     p.item_desc = reinterpret_cast<int*>(c);
     c += align256((size_t)p.max_items * 64);
     p.offsets = reinterpret_cast<int*>(c);
@@ -1028,10 +1050,13 @@ void bind_workspace(Params& p, void* ws) {
     p.records = reinterpret_cast<int*>(c);
 }
 
+hipError_t launch_binned_reset(const Params& p, hipStream_t stream) {
+    return launch_zero(reinterpret_cast<float*>(p.counts), (int64_t)zeroed_ints(p), stream);
+}
+
 hipError_t launch_backward_value_binned(const Params& p0, msda_dtype_t dtype, hipStream_t stream) {
     Params p = p0;
-    hipError_t e = launch_zero(reinterpret_cast<float*>(p.counts), (int64_t)p.n_tiles * 4 + kQueues * kQueueStride, stream);
-    if (e != hipSuccess) return e;
+    hipError_t e = hipSuccess;
     p.q_per_block = kCountQueries / p.K > 0 ? kCountQueries / p.K : 1;
     p.chunks = (p.Lq + p.q_per_block - 1) / p.q_per_block;
     const int bin_blocks = p.n_slabs * p.chunks;
@@ -1040,13 +1065,12 @@ hipError_t launch_backward_value_binned(const Params& p0, msda_dtype_t dtype, hi
     if ((e = hipGetLastError()) != hipSuccess) return e;
     hipLaunchKernelGGL(scan_reduce_kernel, dim3(p.scan_blocks), dim3(256), 0, stream, p);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    hipLaunchKernelGGL(scan_blocks_kernel, dim3(1), dim3(256), 0, stream, p);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
     hipLaunchKernelGGL(scan_apply_kernel, dim3(p.scan_blocks), dim3(256), 0, stream, p);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    hipLaunchKernelGGL(prep_items_kernel, dim3((p.n_tiles + 3) / 4), dim3(256), 0, stream, p);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
-    hipLaunchKernelGGL(bin_scatter_kernel, dim3(bin_blocks), dim3(256), hist_lds, stream, p);
+    // the scatter's workgroups also prepare the work items, at least one wave per four tiles
+    const int prep_blocks = (p.n_tiles + 15) / 16;
+    hipLaunchKernelGGL(bin_scatter_kernel, dim3(bin_blocks > prep_blocks ? bin_blocks : prep_blocks), dim3(256),
+                       hist_lds, stream, p);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     if (p.D % 4 == 0) {
         const int grid = queue_grid();  // the waves take work items from the queue

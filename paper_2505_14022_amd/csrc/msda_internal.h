@@ -60,6 +60,7 @@ struct Params {
     int scan_blocks;            // ceil(n_tiles / kScanTiles)
     int* counts;                // [n_tiles * 4]       samples per (tile, class)
     int* queue;                 // [8 * 64]            fold work queue counters, 256 B apart (zeroed with counts)
+    int* scan_done;             // [1]                 workgroups of the scan's first pass done (zeroed with counts)
     int* item_desc;             // [max_items * 16]    fold work item descriptors
     int* offsets;               // [n_tiles * 4 + 1]   exclusive prefix of counts
     int* cursor;                // [n_tiles * 4]       fill position per bin
@@ -81,6 +82,9 @@ hipError_t launch_prologue_grad(const Params& p, const float* attn, const float*
 // grad_loc / grad_attn; with `atomic_grad_value` the same kernel also scatters grad_value with
 // fp32 atomics (grad_value must be zero beforehand).
 hipError_t launch_backward_grads(const Params& p, msda_dtype_t dtype, bool atomic_grad_value, hipStream_t stream);
+// Zeroes the counters at the head of the binned path's workspace; enqueued before
+// launch_backward_value_binned (on its stream or on one that it waits for).
+hipError_t launch_binned_reset(const Params& p, hipStream_t stream);
 // grad_value by binning samples per destination tile and accumulating each tile once.
 hipError_t launch_backward_value_binned(const Params& p, msda_dtype_t dtype, hipStream_t stream);
 hipError_t launch_zero(float* ptr, int64_t n, hipStream_t stream);
