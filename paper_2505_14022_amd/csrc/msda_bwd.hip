@@ -3,21 +3,29 @@
 //
 // Same mapping as the forward kernel (one (batch, head) slab and a run of queries per workgroup,
 // LPP lanes per query, per-sample descriptions parked in LDS). For each sample every lane forms
-// its channels' share of <g, s>, <g, ds/dw_im> and <g, ds/dh_im> from the four gathered corner
-// rows; the shares are summed over the query's lanes with DPP row operations and written
-// coalesced through LDS. The ATOMIC variant also scatters a * w_corner * g into grad_value with
-// fp32 buffer atomics (the path used when no workspace is given).
+// its channels' share of the four corner dot products G_c = <g, v_c> from the gathered corner rows
+// (the rows of several samples are in flight at once); the shares are summed over the query's
+// lanes with DPP row operations, and <g, s>, <g, ds/dw_im>, <g, ds/dh_im> follow from the four
+// sums. Results are written coalesced through LDS. The ATOMIC variant also scatters
+// a * w_corner * g into grad_value with fp32 buffer atomics (the path used when no workspace is
+// given).
 #include "msda_device.hpp"
 
 namespace msda {
 namespace {
+
+// Samples of one query whose corner rows are loaded together. At the DETR-encoder shape 2 was as
+// fast as 1 and 4 was 30 % slower: the registers of more rows in flight cost resident waves.
+#ifndef MSDA_BWD_UNROLL
+#define MSDA_BWD_UNROLL 1
+#endif
+constexpr int kBwdU = MSDA_BWD_UNROLL;
 
 template <typename T, int VEC, int LPP, bool ATOMIC>
 __global__ __launch_bounds__(kBlock) void bwd_kernel(Params p) {
     constexpr int PPW = 64 / LPP;
     __shared__ int s_lvl[3 * kMaxLevels];
     __shared__ int4 s_off[kWaves][kMaxItems];
-    __shared__ float4 s_w[kWaves][kMaxItems];
     __shared__ float4 s_x[kWaves][kMaxItems];  // {a, lh, lw, -} in, {grad_attn, gx, gy, -} out
     load_levels(p, s_lvl);
 
@@ -49,66 +57,102 @@ __global__ __launch_bounds__(kBlock) void bwd_kernel(Params p) {
             SampleDesc sd;
             describe(p, s_lvl, t.n, t.m, t.q0 + jq, k0 + jk, false, sd);
             s_off[wave][j] = sd.off;
-            s_w[wave][j] = sd.w;
             s_x[wave][j] = make_float4(sd.a, sd.lh, sd.lw, 0.f);
         }
         wave_lds_sync();
         const int base = ps * kn;
-        for (int kk = 0; kk < kn; ++kk) {
-            const int4 off = s_off[wave][base + kk];
-            const float4 w = s_w[wave][base + kk];
-            const float4 x = s_x[wave][base + kk];
-            const float a = x.x, lh = x.y, lw = x.z, hh = 1.f - lh, hw = 1.f - lw;
-            float ga = 0.f, gw = 0.f, gh = 0.f;
+        // kBwdU samples at a time: their 4 * kBwdU corner rows are loaded together, then the sums
+        // over the query's lanes of all of them are formed together
+        for (int kk0 = 0; kk0 < kn; kk0 += kBwdU) {
+            int4 off[kBwdU];
+            float a[kBwdU], lh[kBwdU], lw[kBwdU];
+#pragma unroll
+            for (int u = 0; u < kBwdU; ++u) {
+                const bool act = kk0 + u < kn;
+                const int j = base + (act ? kk0 + u : 0);
+                const int4 o = s_off[wave][j];
+                const float4 x = s_x[wave][j];
+                // a sample past the chunk reads zeros everywhere and is never stored
+                off[u] = act ? o : make_int4(kOOBElem, kOOBElem, kOOBElem, kOOBElem);
+                a[u] = x.x;
+                lh[u] = x.y;
+                lw[u] = x.z;
+            }
+            // per corner c the dot product G_c = <g, v_c>; <g, s> = sum_c w_c G_c, and the
+            // location terms are weighted differences of the G_c
+            float G[kBwdU][4];
+#pragma unroll
+            for (int u = 0; u < kBwdU; ++u)
+#pragma unroll
+                for (int c = 0; c < 4; ++c) G[u][c] = 0.f;
             for (int c0 = 0; c0 < p.D; c0 += LPP * VEC) {
                 const int chan = c0 + sub * VEC;
                 if (chan < p.D) {
                     const uint32_t cb = (uint32_t)chan << Row<T, VEC>::kShift;
-                    float g[VEC], v0[VEC], v1[VEC], v2[VEC], v3[VEC];
+                    float g[VEC];
                     if (one_pass) {
 #pragma unroll
                         for (int i = 0; i < VEC; ++i) g[i] = g_row[i];
                     } else {
                         Row<T, VEC>::load_ptr(g, gout + gout_row + chan);
                     }
-                    Row<T, VEC>::load(v0, vr, ((uint32_t)off.x << Row<T, VEC>::kShift) + cb);
-                    Row<T, VEC>::load(v1, vr, ((uint32_t)off.y << Row<T, VEC>::kShift) + cb);
-                    Row<T, VEC>::load(v2, vr, ((uint32_t)off.z << Row<T, VEC>::kShift) + cb);
-                    Row<T, VEC>::load(v3, vr, ((uint32_t)off.w << Row<T, VEC>::kShift) + cb);
+                    float v[kBwdU][4][VEC];
 #pragma unroll
-                    for (int i = 0; i < VEC; ++i) {
-                        const float s = w.x * v0[i] + w.y * v1[i] + w.z * v2[i] + w.w * v3[i];
-                        ga += g[i] * s;
-                        gw += g[i] * (hh * (v1[i] - v0[i]) + lh * (v3[i] - v2[i]));
-                        gh += g[i] * (hw * (v2[i] - v0[i]) + lw * (v3[i] - v1[i]));
+                    for (int u = 0; u < kBwdU; ++u) {
+                        Row<T, VEC>::load(v[u][0], vr, ((uint32_t)off[u].x << Row<T, VEC>::kShift) + cb);
+                        Row<T, VEC>::load(v[u][1], vr, ((uint32_t)off[u].y << Row<T, VEC>::kShift) + cb);
+                        Row<T, VEC>::load(v[u][2], vr, ((uint32_t)off[u].z << Row<T, VEC>::kShift) + cb);
+                        Row<T, VEC>::load(v[u][3], vr, ((uint32_t)off[u].w << Row<T, VEC>::kShift) + cb);
                     }
+#pragma unroll
+                    for (int u = 0; u < kBwdU; ++u)
+#pragma unroll
+                        for (int c = 0; c < 4; ++c)
+#pragma unroll
+                            for (int i = 0; i < VEC; ++i) G[u][c] += g[i] * v[u][c][i];
                 }
                 if constexpr (ATOMIC) {
                     // grad_value[corner] += a * w_corner * g (fp32 rows). Lane `sub` adds channels
                     // c0 + sub + LPP*i, so each atomic instruction covers LPP contiguous floats of
                     // a row (whole 32- or 64-byte segments) instead of a strided set.
-                    const float a0 = a * w.x, a1 = a * w.y, a2 = a * w.z, a3 = a * w.w;
 #pragma unroll
-                    for (int i = 0; i < VEC; ++i) {
-                        const int ct = c0 + sub + LPP * i;
-                        if (ct < p.D) {
-                            const float gt = (float)gout[gout_row + ct];
-                            const uint32_t ci = (uint32_t)ct << 2;
-                            __builtin_amdgcn_raw_ptr_buffer_atomic_fadd_f32(a0 * gt, gr, ((uint32_t)off.x << 2) + ci, 0, 0);
-                            __builtin_amdgcn_raw_ptr_buffer_atomic_fadd_f32(a1 * gt, gr, ((uint32_t)off.y << 2) + ci, 0, 0);
-                            __builtin_amdgcn_raw_ptr_buffer_atomic_fadd_f32(a2 * gt, gr, ((uint32_t)off.z << 2) + ci, 0, 0);
-                            __builtin_amdgcn_raw_ptr_buffer_atomic_fadd_f32(a3 * gt, gr, ((uint32_t)off.w << 2) + ci, 0, 0);
+                    for (int u = 0; u < kBwdU; ++u) {
+                        if (kk0 + u >= kn) continue;
+                        const float hh = 1.f - lh[u], hw = 1.f - lw[u];
+                        const float a0 = a[u] * (hh * hw), a1 = a[u] * (hh * lw[u]);
+                        const float a2 = a[u] * (lh[u] * hw), a3 = a[u] * (lh[u] * lw[u]);
+#pragma unroll
+                        for (int i = 0; i < VEC; ++i) {
+                            const int ct = c0 + sub + LPP * i;
+                            if (ct < p.D) {
+                                const float gt = (float)gout[gout_row + ct];
+                                const uint32_t ci = (uint32_t)ct << 2;
+                                __builtin_amdgcn_raw_ptr_buffer_atomic_fadd_f32(a0 * gt, gr, ((uint32_t)off[u].x << 2) + ci, 0, 0);
+                                __builtin_amdgcn_raw_ptr_buffer_atomic_fadd_f32(a1 * gt, gr, ((uint32_t)off[u].y << 2) + ci, 0, 0);
+                                __builtin_amdgcn_raw_ptr_buffer_atomic_fadd_f32(a2 * gt, gr, ((uint32_t)off[u].z << 2) + ci, 0, 0);
+                                __builtin_amdgcn_raw_ptr_buffer_atomic_fadd_f32(a3 * gt, gr, ((uint32_t)off[u].w << 2) + ci, 0, 0);
+                            }
                         }
                     }
                 }
             }
-            ga = group_sum<LPP>(ga);
-            gw = group_sum<LPP>(gw);
-            gh = group_sum<LPP>(gh);
+#pragma unroll
+            for (int u = 0; u < kBwdU; ++u)
+#pragma unroll
+                for (int c = 0; c < 4; ++c) G[u][c] = group_sum<LPP>(G[u][c]);
             if (sub == 0) {
-                const int l = (k0 + kk) / p.P;
-                const float Wf = (float)s_lvl[kMaxLevels + l], Hf = (float)s_lvl[l];
-                s_x[wave][base + kk] = make_float4(ga, Wf * (a * gw), Hf * (a * gh), 0.f);
+#pragma unroll
+                for (int u = 0; u < kBwdU; ++u) {
+                    if (kk0 + u >= kn) continue;
+                    const float hh = 1.f - lh[u], hw = 1.f - lw[u];
+                    const float ga = (hh * hw) * G[u][0] + (hh * lw[u]) * G[u][1] + (lh[u] * hw) * G[u][2] +
+                                     (lh[u] * lw[u]) * G[u][3];
+                    const float gw = hh * (G[u][1] - G[u][0]) + lh[u] * (G[u][3] - G[u][2]);
+                    const float gh = hw * (G[u][2] - G[u][0]) + lw[u] * (G[u][3] - G[u][1]);
+                    const int l = (k0 + kk0 + u) / p.P;
+                    const float Wf = (float)s_lvl[kMaxLevels + l], Hf = (float)s_lvl[l];
+                    s_x[wave][base + kk0 + u] = make_float4(ga, Wf * (a[u] * gw), Hf * (a[u] * gh), 0.f);
+                }
             }
         }
         wave_lds_sync();
