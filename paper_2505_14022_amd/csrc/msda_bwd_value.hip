@@ -581,6 +581,24 @@ struct Corners {
     float4 v[4][kQPL];
 };
 
+// In the lanes of `mask` (a wave-wide lane mask): moves the run's sums to `pend` and restarts the
+// run at zero. Written as per-lane selects that update both register sets in place: as C++
+// selects or a branch, the compiler copies all 64 registers on every record.
+__device__ __forceinline__ void park_run(Corners& pend, Corners& run, uint64_t mask) {
+#pragma unroll
+    for (int k = 0; k < 4; ++k)
+#pragma unroll
+        for (int j = 0; j < kQPL; ++j) {
+            float* d = &pend.v[k][j].x;
+            float* r = &run.v[k][j].x;
+#pragma unroll
+            for (int c = 0; c < 4; ++c) {
+                __asm__("v_cndmask_b32_e64 %0, %0, %1, %2" : "+v"(d[c]) : "v"(r[c]), "s"(mask));
+                __asm__("v_cndmask_b32_e64 %0, %0, 0, %1" : "+v"(r[c]) : "s"(mask));
+            }
+        }
+}
+
 // Adds the four corner sums of the run whose top-left corner has key `key` into the LDS tile
 // (pixels outside the tile belong to neighbouring tiles and are dropped). The corners are
 // written one after another, each read-add-write finished before the next begins: another record
@@ -813,8 +831,8 @@ __global__ __launch_bounds__(256, 2) void fold_runs_kernel(Params p) {
                     rk[u] = skey[act ? pos : 0];
                     off[u] = act ? (uint32_t)(e.x + ch) : (uint32_t)kOOBElem;
                     ra[u] = act ? __builtin_bit_cast(float, e.y) : 0.f;
-                    rh[u] = __builtin_bit_cast(float, e.z);
-                    rw[u] = __builtin_bit_cast(float, e.w);
+                    rh[u] = act ? __builtin_bit_cast(float, e.z) : 0.f;
+                    rw[u] = act ? __builtin_bit_cast(float, e.w) : 0.f;
                 }
                 float4 g[kRunBatch][kQPL];
 #pragma unroll
@@ -834,21 +852,21 @@ __global__ __launch_bounds__(256, 2) void fold_runs_kernel(Params p) {
                         if (pkey >= 0) flush_run(acc, pkey, TH, TW, sub, pend);
                         pkey = -1;
                     }
-                    if (ends) {
-                        pend = run;
-                        pkey = cur;
-                        run = Corners{};
-                        cur = key;
+                    // selects rather than a divergent branch, so that `run` keeps its registers
+                    const uint64_t ended = __ballot(ends);
+                    if (ended != 0) {
+                        park_run(pend, run, ended);
+                        pkey = ends ? cur : pkey;
+                        cur = ends ? key : cur;
                     }
-                    if (pos < hi) {
-                        const float lh = rh[u], lw = rw[u], a = ra[u];
-                        const float ah = a * (1.f - lh), al = a * lh, hw = 1.f - lw;
-                        const float wk[4] = {ah * hw, ah * lw, al * hw, al * lw};
+                    // records past the slice have a = 0 and zero rows: they add nothing
+                    const float lh = rh[u], lw = rw[u], a = ra[u];
+                    const float ah = a * (1.f - lh), al = a * lh, hw = 1.f - lw;
+                    const float wk[4] = {ah * hw, ah * lw, al * hw, al * lw};
 #pragma unroll
-                        for (int k = 0; k < 4; ++k)
+                    for (int k = 0; k < 4; ++k)
 #pragma unroll
-                            for (int j = 0; j < kQPL; ++j) add4(run.v[k][j], wk[k], g[u][j]);
-                    }
+                        for (int j = 0; j < kQPL; ++j) add4(run.v[k][j], wk[k], g[u][j]);
                 }
             }
             // the finished runs still waiting (their keys differ: each ended inside its own slice)
