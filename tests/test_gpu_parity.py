@@ -61,6 +61,14 @@ def test_dense_coarse_levels_split_tiles(seed):
     check_parity(inp, workspace="owner")
 
 
+def test_many_tiles_multi_pass_scan():
+    # 128 slabs x 525 tiles: the bin scan runs over more than 256 workgroups (the last one scans
+    # their totals in several passes), and most of the scatter's workgroups only prepare work items
+    inp = workloads.random_case(16, 8, 4, ((168, 200),), 2, 48, "f32", seed=77)
+    say("many tiles: multi-pass scan of workgroup totals")
+    check_parity(inp, workspace="owner")
+
+
 @pytest.mark.parametrize("lo,hi", [(-0.6, 1.6), (0.0, 1.0), (0.45, 0.55)])
 def test_location_ranges(lo, hi):
     inp = workloads.random_case(2, 4, 32, ((13, 17), (7, 9)), 4, 123, "f32", seed=7, lo=lo, hi=hi)
