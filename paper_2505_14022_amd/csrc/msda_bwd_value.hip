@@ -76,6 +76,8 @@ __device__ __forceinline__ int level_of_tile(const int* g, int L, int tin) {
 
 // ---------------------------------------------------------------- 1. count
 
+constexpr int kBinRounds = kCountQueries / 256;  // samples per thread in the count / scatter passes
+
 __global__ __launch_bounds__(256) void bin_count_kernel(Params p) {
     extern __shared__ int hist[];  // bins of this slab
     __shared__ int s_geo[kGeo * kMaxLevels];
@@ -88,10 +90,24 @@ __global__ __launch_bounds__(256) void bin_count_kernel(Params p) {
     const int nq = min(p.q_per_block, p.Lq - q0);
     const int nsamp = nq * p.K;
     const float2* loc = reinterpret_cast<const float2*>(p.loc);
-    for (int j = threadIdx.x; j < nsamp; j += 256) {
-        const int jq = j / p.K, k = j - jq * p.K;
-        const int smp = ((n * p.Lq + q0 + jq) * p.M + m) * p.K + k;
-        const int b = sample_bin(s_geo, k / p.P, loc[smp]);
+    // all of a thread's locations are loaded before any is binned, so their loads are in flight
+    // together (nsamp <= kCountQueries = 256 * kBinRounds)
+    float2 xy[kBinRounds];
+    int lvl[kBinRounds];
+#pragma unroll
+    for (int r = 0; r < kBinRounds; ++r) {
+        const int j = threadIdx.x + 256 * r;
+        xy[r] = make_float2(-2.f, -2.f);  // off the map
+        lvl[r] = 0;
+        if (j < nsamp) {
+            const int jq = j / p.K, k = j - jq * p.K;
+            xy[r] = loc[((n * p.Lq + q0 + jq) * p.M + m) * p.K + k];
+            lvl[r] = k / p.P;
+        }
+    }
+#pragma unroll
+    for (int r = 0; r < kBinRounds; ++r) {
+        const int b = sample_bin(s_geo, lvl[r], xy[r]);
         if (b >= 0) atomicAdd(&hist[b], 1);
     }
     __syncthreads();
@@ -302,8 +318,6 @@ __device__ __forceinline__ void prep_tile(const Params& p, const int* s_geo, int
 
 // ---------------------------------------------------------------- 3. scatter
 
-constexpr int kScatterRounds = kCountQueries / 256;
-
 // Records of one workgroup's (slab, chunk of queries): ranks within the workgroup from LDS
 // counters, one global atomic per bin for the workgroup's base, then the record stores.
 __device__ __forceinline__ void scatter_chunk(const Params& p, const int* s_geo, int* hist, int bps) {
@@ -313,26 +327,37 @@ __device__ __forceinline__ void scatter_chunk(const Params& p, const int* s_geo,
     const int nq = min(p.q_per_block, p.Lq - q0);
     const int nsamp = nq * p.K;
     const float2* loc = reinterpret_cast<const float2*>(p.loc);
-    int bins[kScatterRounds], ranks[kScatterRounds];
-    int4 rec[kScatterRounds];  // {grad_out row, a, h_im, w_im}: everything the fold needs
+    int bins[kBinRounds], ranks[kBinRounds];
+    int4 rec[kBinRounds];  // {grad_out row, a, h_im, w_im}: everything the fold needs
+    // every load first (all in flight together), then the bins and ranks
+    float2 xy[kBinRounds];
+    int lvl[kBinRounds];
 #pragma unroll
-    for (int r = 0; r < kScatterRounds; ++r) {
+    for (int r = 0; r < kBinRounds; ++r) {
         const int j = threadIdx.x + 256 * r;
-        bins[r] = -1;
-        ranks[r] = 0;
+        xy[r] = make_float2(-2.f, -2.f);  // off the map
+        lvl[r] = 0;
         rec[r] = make_int4(0, 0, 0, 0);
         if (j < nsamp) {
             const int jq = j / p.K, k = j - jq * p.K;
             const int pair = (n * p.Lq + q0 + jq) * p.M + m;
             const int smp = pair * p.K + k;
-            float h_im, w_im;
-            const int b = sample_bin(s_geo, k / p.P, loc[smp], &h_im, &w_im);
-            bins[r] = b;
-            if (b >= 0) {
-                ranks[r] = atomicAdd(&hist[b], 1);
-                rec[r] = make_int4(pair * p.D, __builtin_bit_cast(int, p.attn[smp]), __builtin_bit_cast(int, h_im),
-                                   __builtin_bit_cast(int, w_im));
-            }
+            xy[r] = loc[smp];
+            lvl[r] = k / p.P;
+            rec[r].x = pair * p.D;
+            rec[r].y = __builtin_bit_cast(int, p.attn[smp]);
+        }
+    }
+#pragma unroll
+    for (int r = 0; r < kBinRounds; ++r) {
+        float h_im, w_im;
+        const int b = sample_bin(s_geo, lvl[r], xy[r], &h_im, &w_im);
+        bins[r] = b;
+        ranks[r] = 0;
+        if (b >= 0) {
+            ranks[r] = atomicAdd(&hist[b], 1);
+            rec[r].z = __builtin_bit_cast(int, h_im);
+            rec[r].w = __builtin_bit_cast(int, w_im);
         }
     }
     __syncthreads();
@@ -344,7 +369,7 @@ __device__ __forceinline__ void scatter_chunk(const Params& p, const int* s_geo,
     __syncthreads();
     int4* records = reinterpret_cast<int4*>(p.records);
 #pragma unroll
-    for (int r = 0; r < kScatterRounds; ++r) {
+    for (int r = 0; r < kBinRounds; ++r) {
         if (bins[r] < 0) continue;
         const int pos = hist[bins[r]] + ranks[r];
         if (pos < p.n_samples) records[pos] = rec[r];  // always true when counts and cursor agree
