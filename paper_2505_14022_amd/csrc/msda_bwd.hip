@@ -26,7 +26,7 @@ __global__ __launch_bounds__(kBlock) void bwd_kernel(Params p) {
     constexpr int PPW = 64 / LPP;
     __shared__ int s_lvl[3 * kMaxLevels];
     __shared__ int4 s_off[kWaves][kMaxItems];
-    __shared__ float4 s_x[kWaves][kMaxItems];  // {a, lh, lw, -} in, {grad_attn, gx, gy, -} out
+    __shared__ float4 s_x[kWaves][kMaxItems];  // {a, lh, lw, -} of each sample
     load_levels(p, s_lvl);
 
     Tile t;
@@ -140,30 +140,37 @@ __global__ __launch_bounds__(kBlock) void bwd_kernel(Params p) {
             for (int u = 0; u < kBwdU; ++u)
 #pragma unroll
                 for (int c = 0; c < 4; ++c) G[u][c] = group_sum<LPP>(G[u][c]);
+            // the four sums replace the sample's corner offsets in LDS (every lane has read them:
+            // a wave's LDS operations complete in order)
             if (sub == 0) {
 #pragma unroll
-                for (int u = 0; u < kBwdU; ++u) {
-                    if (kk0 + u >= kn) continue;
-                    const float hh = 1.f - lh[u], hw = 1.f - lw[u];
-                    const float ga = (hh * hw) * G[u][0] + (hh * lw[u]) * G[u][1] + (lh[u] * hw) * G[u][2] +
-                                     (lh[u] * lw[u]) * G[u][3];
-                    const float gw = hh * (G[u][1] - G[u][0]) + lh[u] * (G[u][3] - G[u][2]);
-                    const float gh = hw * (G[u][2] - G[u][0]) + lw[u] * (G[u][3] - G[u][1]);
-                    const int l = (k0 + kk0 + u) / p.P;
-                    const float Wf = (float)s_lvl[kMaxLevels + l], Hf = (float)s_lvl[l];
-                    s_x[wave][base + kk0 + u] = make_float4(ga, Wf * (a[u] * gw), Hf * (a[u] * gh), 0.f);
-                }
+                for (int u = 0; u < kBwdU; ++u)
+                    if (kk0 + u < kn)
+                        s_off[wave][base + kk0 + u] =
+                            make_int4(__builtin_bit_cast(int, G[u][0]), __builtin_bit_cast(int, G[u][1]),
+                                      __builtin_bit_cast(int, G[u][2]), __builtin_bit_cast(int, G[u][3]));
             }
         }
         wave_lds_sync();
+        // one sample per lane: <g, s> = sum_c w_c G_c, and the location terms are weighted
+        // differences of the G_c, scaled by the attention weight and the level size
         for (int j = lane; j < PPW * kn; j += 64) {
             const int jq = j / kn, jk = j - jq * kn;
             const int q = t.q0 + jq;
             if (q < p.Lq) {
+                const int4 gi = s_off[wave][j];
+                const float G0 = __builtin_bit_cast(float, gi.x), G1 = __builtin_bit_cast(float, gi.y);
+                const float G2 = __builtin_bit_cast(float, gi.z), G3 = __builtin_bit_cast(float, gi.w);
+                const float4 x = s_x[wave][j];
+                const float a = x.x, lh = x.y, lw = x.z, hh = 1.f - lh, hw = 1.f - lw;
+                const float ga = (hh * hw) * G0 + (hh * lw) * G1 + (lh * hw) * G2 + (lh * lw) * G3;
+                const float gw = hh * (G1 - G0) + lh * (G3 - G2);
+                const float gh = hw * (G2 - G0) + lw * (G3 - G1);
+                const int l = (k0 + jk) / p.P;
+                const float Wf = (float)s_lvl[kMaxLevels + l], Hf = (float)s_lvl[l];
                 const int smp = ((t.n * p.Lq + q) * p.M + t.m) * K + k0 + jk;
-                const float4 r = s_x[wave][j];
-                p.grad_attn[smp] = r.x;
-                reinterpret_cast<float2*>(p.grad_loc)[smp] = make_float2(r.y, r.z);
+                p.grad_attn[smp] = ga;
+                reinterpret_cast<float2*>(p.grad_loc)[smp] = make_float2(Wf * (a * gw), Hf * (a * gh));
             }
         }
     }
