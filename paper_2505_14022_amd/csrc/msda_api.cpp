@@ -202,12 +202,21 @@ msda_status_t backward_body(const void* value, const int64_t* shapes, const int6
         p.value_bytes = (uint32_t)(cnt * S * M * D * es);
         p.gv_bytes = (uint32_t)(cnt * S * M * D * 4);
         hipError_t e = hipSuccess;
+        // fused entry points: the backward kernel forms grad_offsets and grad_logits itself when it
+        // holds all of a query's samples at once, else they follow from staged grad_loc / grad_attn
+        const bool grads_in_kernel = pro && msda::prologue_grads_in_kernel(p, (msda_dtype_t)dtype);
         if (pro) {
             p.ref = pro->ref + n0 * Lq * L * 2;
             p.pix_offsets = pro->offsets + n0 * Lq * M * L * P * 2;
             p.logits = pro->logits + n0 * Lq * M * L * P;
             e = msda::launch_prologue(p, const_cast<float*>(p.loc), const_cast<float*>(p.attn), s);
             if (e != hipSuccess) return fail(MSDA_ERROR_LAUNCH_FAILED, "prologue launch: %s", hipGetErrorString(e));
+        }
+        if (grads_in_kernel) {
+            const int64_t q0 = n0 * Lq * M * L * P;
+            p.prologue_grads = 1;
+            p.grad_loc = pro->grad_offsets + q0 * 2;
+            p.grad_attn = pro->grad_logits + q0;
         }
         if (binned) {
             if (!msda::plan_binned(p))
@@ -229,7 +238,12 @@ msda_status_t backward_body(const void* value, const int64_t* shapes, const int6
         }
         e = msda::launch_backward_grads(p, (msda_dtype_t)dtype, !binned, s);
         if (e != hipSuccess) return fail(MSDA_ERROR_LAUNCH_FAILED, "backward launch: %s", hipGetErrorString(e));
-        if (pro) {
+        if (grads_in_kernel) {
+            if (pro->grad_ref &&
+                (e = msda::launch_ref_grad_from_offsets(p, p.grad_loc, pro->grad_ref + n0 * Lq * L * 2, s)) !=
+                    hipSuccess)
+                return fail(MSDA_ERROR_LAUNCH_FAILED, "grad_ref launch: %s", hipGetErrorString(e));
+        } else if (pro) {
             const int64_t q0 = n0 * Lq * M * L * P;
             e = msda::launch_prologue_grad(p, p.attn, p.grad_loc, p.grad_attn, pro->grad_offsets + q0 * 2,
                                            pro->grad_logits + q0,

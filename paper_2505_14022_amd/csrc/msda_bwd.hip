@@ -166,11 +166,35 @@ __global__ __launch_bounds__(kBlock) void bwd_kernel(Params p) {
                 const float ga = (hh * hw) * G0 + (hh * lw) * G1 + (lh * hw) * G2 + (lh * lw) * G3;
                 const float gw = hh * (G1 - G0) + lh * (G3 - G2);
                 const float gh = hw * (G2 - G0) + lw * (G3 - G1);
-                const int l = (k0 + jk) / p.P;
-                const float Wf = (float)s_lvl[kMaxLevels + l], Hf = (float)s_lvl[l];
                 const int smp = ((t.n * p.Lq + q) * p.M + t.m) * K + k0 + jk;
-                p.grad_attn[smp] = ga;
-                reinterpret_cast<float2*>(p.grad_loc)[smp] = make_float2(Wf * (a * gw), Hf * (a * gh));
+                if (p.prologue_grads) {
+                    // the offsets are in pixels of the level: d loc / d offset = 1 / (W_l, H_l), which
+                    // cancels the level size of grad_loc
+                    reinterpret_cast<float2*>(p.grad_loc)[smp] = make_float2(a * gw, a * gh);
+                    s_x[wave][j] = make_float4(a, ga, a * ga, 0.f);
+                } else {
+                    const int l = (k0 + jk) / p.P;
+                    const float Wf = (float)s_lvl[kMaxLevels + l], Hf = (float)s_lvl[l];
+                    p.grad_attn[smp] = ga;
+                    reinterpret_cast<float2*>(p.grad_loc)[smp] = make_float2(Wf * (a * gw), Hf * (a * gh));
+                }
+            }
+        }
+        if (p.prologue_grads) {
+            // softmax chain rule over the query's kn = K samples (all in this chunk):
+            // d loss / d logit_k = a_k (grad_attn_k - sum_i a_i grad_attn_i)
+            wave_lds_sync();
+            for (int j = lane; j < PPW * kn; j += 64) {
+                const int jq = j / kn, jk = j - jq * kn;
+                const int q = t.q0 + jq;
+                if (q < p.Lq) {
+                    float dot = 0.f;
+                    for (int i = 0; i < kn; ++i) dot += s_x[wave][jq * kn + i].z;
+                    // the weight itself, also where the sample is off the map (there grad_attn = 0
+                    // but the softmax still ties its logit to the others)
+                    const int smp = ((t.n * p.Lq + q) * p.M + t.m) * K + k0 + jk;
+                    p.grad_attn[smp] = p.attn[smp] * (s_x[wave][j].y - dot);
+                }
             }
         }
     }
@@ -199,6 +223,12 @@ hipError_t launch_backward_grads(const Params& p, msda_dtype_t dtype, bool atomi
         return dtype == MSDA_F16 ? launch_typed<BwdAtomicK, _Float16>(p, stream)
                                  : launch_typed<BwdAtomicK, float>(p, stream);
     return dtype == MSDA_F16 ? launch_typed<BwdK, _Float16>(p, stream) : launch_typed<BwdK, float>(p, stream);
+}
+
+bool prologue_grads_in_kernel(const Params& p, msda_dtype_t dtype) {
+    const int vec = dtype == MSDA_F16 ? pick_vec<_Float16>(p.D) : pick_vec<float>(p.D);
+    const int ppw = 64 / pick_lpp(p.D, vec);  // queries per wave, as launch_lpp picks them
+    return p.K <= kMaxItems / ppw;            // the kernel's chunk of samples per query is all of K
 }
 
 hipError_t launch_zero(float* ptr, int64_t n, hipStream_t stream) {

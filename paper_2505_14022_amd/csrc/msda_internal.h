@@ -39,6 +39,7 @@ struct Params {
     float* grad_value;     // [n_batch, S, M, D] fp32                        (backward)
     float* grad_loc;       // [n_batch, Lq, M, L, P, 2]                      (backward)
     float* grad_attn;      // [n_batch, Lq, M, L, P]                         (backward)
+    int prologue_grads;    // backward: grad_loc / grad_attn hold grad_offsets / grad_logits instead
     uint32_t value_bytes;  // size of the value buffer resource
     uint32_t gv_bytes;     // size of the grad_value buffer resource
     int n_batch, S, M, D, Lq, L, P, K;  // K = L*P samples per (query, head)
@@ -80,8 +81,16 @@ hipError_t launch_prologue_grad(const Params& p, const float* attn, const float*
                                 const float* grad_attn, float* grad_offsets, float* grad_logits,
                                 float* grad_ref, hipStream_t stream);
 // grad_loc / grad_attn; with `atomic_grad_value` the same kernel also scatters grad_value with
-// fp32 atomics (grad_value must be zero beforehand).
+// fp32 atomics (grad_value must be zero beforehand). With p.prologue_grads set, the kernel writes the
+// prologue's gradients instead (grad_offsets into p.grad_loc, grad_logits into p.grad_attn); that
+// needs prologue_grads_in_kernel(p, dtype).
 hipError_t launch_backward_grads(const Params& p, msda_dtype_t dtype, bool atomic_grad_value, hipStream_t stream);
+// True when the backward kernel holds all L*P samples of a (query, head) at once, so that it can
+// form the softmax chain rule of the fused entry points itself.
+bool prologue_grads_in_kernel(const Params& p, msda_dtype_t dtype);
+// grad_ref from grad_offsets (grad_loc = grad_offsets * (W_l, H_l), summed over heads and points).
+hipError_t launch_ref_grad_from_offsets(const Params& p, const float* grad_offsets, float* grad_ref,
+                                        hipStream_t stream);
 // Zeroes the counters at the head of the binned path's workspace; enqueued before
 // launch_backward_value_binned (on its stream or on one that it waits for).
 hipError_t launch_binned_reset(const Params& p, hipStream_t stream);

@@ -119,7 +119,36 @@ __global__ __launch_bounds__(256) void ref_grad_kernel(Params p, const float* gr
     reinterpret_cast<float2*>(grad_ref)[i] = make_float2(gx, gy);
 }
 
+// As ref_grad_kernel, from grad_offsets: grad_loc = grad_offsets * (W_l, H_l), the same fp32
+// product the backward kernel forms for grad_loc.
+__global__ __launch_bounds__(256) void ref_grad_offsets_kernel(Params p, const float* grad_off, float* grad_ref) {
+    __shared__ int s_lvl[3 * kMaxLevels];
+    load_levels(p, s_lvl);
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;  // (n, q, l)
+    if (i >= (int64_t)p.n_batch * p.Lq * p.L) return;
+    const int l = (int)(i % p.L);
+    const float Wf = (float)s_lvl[kMaxLevels + l], Hf = (float)s_lvl[l];
+    const int64_t nq = i / p.L;
+    float gx = 0.f, gy = 0.f;
+    for (int m = 0; m < p.M; ++m)
+        for (int pt = 0; pt < p.P; ++pt) {
+            const float2 g = reinterpret_cast<const float2*>(grad_off)[(nq * p.M + m) * p.K + l * p.P + pt];
+            gx += Wf * g.x;
+            gy += Hf * g.y;
+        }
+    reinterpret_cast<float2*>(grad_ref)[i] = make_float2(gx, gy);
+}
+
 }  // namespace
+
+hipError_t launch_ref_grad_from_offsets(const Params& p, const float* grad_offsets, float* grad_ref,
+                                        hipStream_t stream) {
+    const int64_t r = (int64_t)p.n_batch * p.Lq * p.L;
+    if (r == 0) return hipSuccess;
+    hipLaunchKernelGGL(ref_grad_offsets_kernel, dim3((unsigned)((r + 255) / 256)), dim3(256), 0, stream, p,
+                       grad_offsets, grad_ref);
+    return hipGetLastError();
+}
 
 hipError_t launch_prologue(const Params& p, float* loc, float* attn, hipStream_t stream) {
     if ((int64_t)p.n_batch * p.Lq * p.M == 0) return hipSuccess;
