@@ -27,7 +27,9 @@
 namespace msda {
 namespace {
 
-constexpr int kGeo = 7;  // per-level table in LDS: H, W, log2 tile h, log2 tile w, tiles_x, tile_base, start
+// per-level table in LDS: H, W, log2 tile h, log2 tile w, tiles_x, tile_base, start, bins per tile,
+// first bin of the level within a slab
+constexpr int kGeo = 9;
 constexpr int kAccWaves = 4;
 
 __device__ __forceinline__ void load_geo(const Params& p, int* s) {
@@ -41,11 +43,35 @@ __device__ __forceinline__ void load_geo(const Params& p, int* s) {
         s[4 * kMaxLevels + l] = in ? p.tiles_x[l] : 1;
         s[5 * kMaxLevels + l] = in ? p.tile_base[l] : 0x7fffffff;
         s[6 * kMaxLevels + l] = in ? p.start[l] : 0;
+        s[7 * kMaxLevels + l] = in ? p.tile_bins[l] : 4;
+        s[8 * kMaxLevels + l] = in ? p.bin_base[l] : 0;
     }
     __syncthreads();
 }
 
-// Bin of a sample within its slab (tile * 4 + class), or -1 if the sample is off the map.
+// Bins of a tile. A sample goes to the tile of its top-left corner, into one of four classes by the
+// neighbouring tiles its other corners reach: interior, right, right+down, down (in this order, so
+// that the left neighbour's visible records (right, right+down), the upper one's (right+down, down)
+// and the upper-left one's (right+down) are contiguous bin ranges). With B = 4 bins a tile has one
+// bin per class. Dense levels use B = 4 + 7 bins: the interior class is split by the row of the
+// top-left corner in the tile, so a tile's records are ordered by row and a work item cut from them
+// sees few distinct corner positions.
+constexpr int kKeyedBins = 11;
+__device__ __forceinline__ int bin_in_tile(int B, int cls, int row) {
+    return cls == 0 ? (B == 4 ? 0 : row) : B - 4 + cls;
+}
+
+// First bin of tile t (global tile index), and its bin count.
+__device__ __forceinline__ int tile_bin0(const Params& p, const int* g, int t, int& B) {
+    const int slab = t / p.tiles_per_slab, tin = t - slab * p.tiles_per_slab;
+    int l = 0;
+    for (int i = 1; i < p.L; ++i)
+        if (tin >= g[5 * kMaxLevels + i]) l = i;
+    B = g[7 * kMaxLevels + l];
+    return slab * p.bins_per_slab + g[8 * kMaxLevels + l] + (tin - g[5 * kMaxLevels + l]) * B;
+}
+
+// Bin of a sample within its slab, or -1 if the sample is off the map.
 // Uses the same fp32 coordinates as every other kernel, so the bin agrees with the corners.
 __device__ __forceinline__ int sample_bin(const int* g, int l, float2 xy, float* h_out = nullptr,
                                           float* w_out = nullptr) {
@@ -63,8 +89,9 @@ __device__ __forceinline__ int sample_bin(const int* g, int l, float2 xy, float*
     const bool right = w0 >= 0 && (w0 & mw) == mw && w0 + 1 < W;
     const bool down = h0 >= 0 && (h0 & mh) == mh && h0 + 1 < H;
     const int cls = right ? (down ? 2 : 1) : (down ? 3 : 0);
-    const int tile = g[5 * kMaxLevels + l] + (hc >> th) * g[4 * kMaxLevels + l] + (wc >> tw);
-    return tile * 4 + cls;
+    const int B = g[7 * kMaxLevels + l];
+    const int tl = (hc >> th) * g[4 * kMaxLevels + l] + (wc >> tw);  // tile within the level
+    return g[8 * kMaxLevels + l] + tl * B + bin_in_tile(B, cls, hc & mh);
 }
 
 __device__ __forceinline__ int level_of_tile(const int* g, int L, int tin) {
@@ -81,7 +108,7 @@ constexpr int kBinRounds = kCountQueries / 256;  // samples per thread in the co
 __global__ __launch_bounds__(256) void bin_count_kernel(Params p) {
     extern __shared__ int hist[];  // bins of this slab
     __shared__ int s_geo[kGeo * kMaxLevels];
-    const int bps = p.tiles_per_slab * 4;
+    const int bps = p.bins_per_slab;
     for (int i = threadIdx.x; i < bps; i += 256) hist[i] = 0;
     load_geo(p, s_geo);
     const int slab = blockIdx.x / p.chunks, chunk = blockIdx.x - slab * p.chunks;
@@ -134,21 +161,24 @@ __device__ __forceinline__ TileInfo tile_info(const Params& p, const int* g, int
     const int rel = tin - g[5 * kMaxLevels + l];
     const int tx_n = g[4 * kMaxLevels + l];
     const int ty = rel / tx_n, tx = rel - ty * tx_n;
+    // the tiles of one level have the same bin count B and consecutive bins
+    const int B = g[7 * kMaxLevels + l];
+    const int b0 = (t / p.tiles_per_slab) * p.bins_per_slab + g[8 * kMaxLevels + l] + rel * B;
     TileInfo ti;
-    ti.own0 = 4 * t;
-    ti.own1 = 4 * t + 4;
+    ti.own0 = b0;
+    ti.own1 = b0 + B;
     ti.l0 = ti.l1 = ti.u0 = ti.u1 = ti.d0 = ti.d1 = 0;
     if (tx > 0) {
-        ti.l0 = 4 * (t - 1) + 1;
-        ti.l1 = 4 * (t - 1) + 3;
+        ti.l0 = b0 - B + B - 3;
+        ti.l1 = b0 - B + B - 1;
     }
     if (ty > 0) {
-        ti.u0 = 4 * (t - tx_n) + 2;
-        ti.u1 = 4 * (t - tx_n) + 4;
+        ti.u0 = b0 - tx_n * B + B - 2;
+        ti.u1 = b0 - tx_n * B + B;
     }
     if (tx > 0 && ty > 0) {
-        ti.d0 = 4 * (t - tx_n - 1) + 2;
-        ti.d1 = 4 * (t - tx_n - 1) + 3;
+        ti.d0 = b0 - (tx_n + 1) * B + B - 2;
+        ti.d1 = b0 - (tx_n + 1) * B + B - 1;
     }
     return ti;
 }
@@ -261,16 +291,18 @@ __global__ __launch_bounds__(256) void scan_apply_kernel(Params p) {
     for (int i = 0; i < kTilesPerThread; ++i) {
         const int t = t0 + i;
         if (t >= p.n_tiles) break;
-        for (int c = 0; c < 4; ++c) {
-            p.offsets[4 * t + c] = rec;
-            p.cursor[4 * t + c] = rec;
-            rec += p.counts[4 * t + c];
+        int B;
+        const int b0 = tile_bin0(p, s_geo, t, B);
+        for (int c = 0; c < B; ++c) {
+            p.offsets[b0 + c] = rec;
+            p.cursor[b0 + c] = rec;
+            rec += p.counts[b0 + c];
         }
         p.tile_chunks[t] = item;
         for (int c = 0; c < items[i] && item + c < p.max_items; ++c) p.items[item + c] = t;
         item += items[i];
         if (t == p.n_tiles - 1) {
-            p.offsets[4 * p.n_tiles] = rec;
+            p.offsets[p.n_bins] = rec;
             p.tile_chunks[p.n_tiles] = item < p.max_items ? item : p.max_items;
         }
     }
@@ -380,7 +412,7 @@ __device__ __forceinline__ void scatter_chunk(const Params& p, const int* s_geo,
 __global__ __launch_bounds__(256) void bin_scatter_kernel(Params p) {
     extern __shared__ int hist[];  // bins of this slab
     __shared__ int s_geo[kGeo * kMaxLevels];
-    const int bps = p.tiles_per_slab * 4;
+    const int bps = p.bins_per_slab;
     for (int i = threadIdx.x; i < bps; i += 256) hist[i] = 0;
     load_geo(p, s_geo);
     if (blockIdx.x < p.n_slabs * p.chunks) scatter_chunk(p, s_geo, hist, bps);
@@ -933,7 +965,8 @@ __global__ __launch_bounds__(256, 2) void fold_runs_kernel(Params p) {
                     const int px = e / (4 * kPixQ), cc = e - px * (4 * kPixQ);
                     const int r = px >> tw, c = px & (TW - 1);
                     const float v = accf[e];
-                    if (px < TH * TW && r < th_on && c < tw_on && ch0 + cc < D) {
+                    // a work item of a split tile reaches few of its pixels: zeros are not added
+                    if (v != 0.f && px < TH * TW && r < th_on && c < tw_on && ch0 + cc < D) {
                         float* dst = p.grad_value + ((size_t)(n * p.S + st + (h_org + r) * W + w_org + c) * p.M + m) * D +
                                      ch0 + cc;
                         unsafeAtomicAdd(dst, v);
@@ -996,7 +1029,7 @@ bool plan_binned(Params& p) {
     for (;;) {
         int64_t tps = 0;
         for (int l = 0; l < p.L; ++l) tps += tiles_of(l);
-        if (tps * 4 <= kHistMax) break;
+        if (tps * 4 <= kHistMax) break;  // bins of a slab at 4 per tile
         // coarsen the level with the most tiles that can still grow
         int best = -1;
         int64_t most = 0;
@@ -1024,11 +1057,42 @@ bool plan_binned(Params& p) {
         }
     }
     p.tiles_per_slab = base;
+    // Bins per tile: levels whose tiles see more records than one work item folds get the interior
+    // class split by row (kKeyedBins per tile), densest first while a slab's bins fit the histogram.
+    int B[kMaxLevels];
+    double dens[kMaxLevels];
+    for (int l = 0; l < p.L; ++l) {
+        B[l] = 4;
+        // visible records of an 8 x 8 tile if the samples were spread evenly: own + ~27 % straddling
+        dens[l] = runs ? 1.27 * 64.0 * p.Lq * p.P / ((double)p.H[l] * p.W[l]) : 0.0;
+    }
+    int64_t bins = 4 * (int64_t)base;
+    for (;;) {
+        int best = -1;
+        for (int l = 0; l < p.L; ++l)
+            if (B[l] == 4 && dens[l] > kChunkRecords && (best < 0 || dens[l] > dens[best])) best = l;
+        if (best < 0) break;
+        const int64_t more = (kKeyedBins - 4) * tiles_of(best);
+        if (bins + more <= kHistMax) {
+            B[best] = kKeyedBins;
+            bins += more;
+        }
+        dens[best] = 0.0;  // decided
+    }
+    int bbase = 0;
+    for (int l = 0; l < kMaxLevels; ++l) {
+        p.tile_bins[l] = l < p.L ? B[l] : 4;
+        p.bin_base[l] = bbase;
+        if (l < p.L) bbase += B[l] * (int)tiles_of(l);
+    }
+    p.bins_per_slab = bbase;
     const int64_t n_slabs = (int64_t)p.n_batch * p.M;
     const int64_t n_tiles = n_slabs * base;
+    const int64_t n_bins = n_slabs * bbase;
     const int64_t n_samples = (int64_t)p.n_batch * p.Lq * p.M * p.K;
     const int64_t max_items = 2 * n_tiles + 4 * n_samples / kChunkRecords + 1;
-    if (n_tiles * 4 + 1 > kMaxIndex || max_items > kMaxIndex || n_samples > kMaxIndex) return false;
+    if (n_bins + 1 > kMaxIndex || max_items > kMaxIndex || n_samples > kMaxIndex) return false;
+    p.n_bins = (int)n_bins;
     p.n_slabs = (int)n_slabs;
     p.n_tiles = (int)n_tiles;
     p.n_samples = (int)n_samples;
@@ -1061,10 +1125,10 @@ int queue_grid() {
 
 // Ints of the workspace's zeroed head: the per-bin counts, the fold's queue counters and the scan's
 // count of finished workgroups, each counter on a 256-byte line of its own.
-size_t zeroed_ints(const Params& p) { return (size_t)p.n_tiles * 4 + (kQueues + 1) * kQueueStride; }
+size_t zeroed_ints(const Params& p) { return (size_t)p.n_bins + (kQueues + 1) * kQueueStride; }
 
 size_t binned_workspace_bytes(const Params& p) {
-    const size_t nb = (size_t)p.n_tiles * 4;
+    const size_t nb = (size_t)p.n_bins;
     return align256(zeroed_ints(p) * 4) + align256((size_t)p.max_items * 64) + align256((nb + 1) * 4) + align256(nb * 4) +
            align256(((size_t)p.n_tiles + 1) * 4) +
            align256((size_t)p.max_items * 4) + align256((size_t)p.scan_blocks * 2 * 4) +
@@ -1073,7 +1137,7 @@ size_t binned_workspace_bytes(const Params& p) {
 
 void bind_workspace(Params& p, void* ws) {
     char* c = static_cast<char*>(ws);
-    const size_t nb = (size_t)p.n_tiles * 4;
+    const size_t nb = (size_t)p.n_bins;
     p.counts = reinterpret_cast<int*>(c);
     p.queue = p.counts + nb;
     p.scan_done = p.queue + kQueues * kQueueStride;
@@ -1103,7 +1167,7 @@ hipError_t launch_backward_value_binned(const Params& p0, msda_dtype_t dtype, hi
     p.q_per_block = kCountQueries / p.K > 0 ? kCountQueries / p.K : 1;
     p.chunks = (p.Lq + p.q_per_block - 1) / p.q_per_block;
     const int bin_blocks = p.n_slabs * p.chunks;
-    const size_t hist_lds = (size_t)p.tiles_per_slab * 4 * sizeof(int);
+    const size_t hist_lds = (size_t)p.bins_per_slab * sizeof(int);
     hipLaunchKernelGGL(bin_count_kernel, dim3(bin_blocks), dim3(256), hist_lds, stream, p);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     hipLaunchKernelGGL(scan_reduce_kernel, dim3(p.scan_blocks), dim3(256), 0, stream, p);

@@ -53,18 +53,22 @@ struct Params {
     int tile_lw[kMaxLevels];    // log2 of the tile width at level l
     int tiles_x[kMaxLevels];    // tiles per tile-row at level l
     int tile_base[kMaxLevels];  // first tile of level l within a slab
+    int tile_bins[kMaxLevels];  // bins per tile at level l (4, or 11 with the interior class split by row)
+    int bin_base[kMaxLevels];   // first bin of level l within a slab
     int tiles_per_slab;
+    int bins_per_slab;
+    int n_bins;                 // n_slabs * bins_per_slab
     int n_slabs;                // n_batch * M
     int n_tiles;                // n_slabs * tiles_per_slab
     int n_samples;              // n_batch * Lq * M * K
     int max_items;              // capacity of `items`
     int scan_blocks;            // ceil(n_tiles / kScanTiles)
-    int* counts;                // [n_tiles * 4]       samples per (tile, class)
+    int* counts;                // [n_bins]            samples per bin (tile, class)
     int* queue;                 // [8 * 64]            fold work queue counters, 256 B apart (zeroed with counts)
     int* scan_done;             // [1]                 workgroups of the scan's first pass done (zeroed with counts)
     int* item_desc;             // [max_items * 16]    fold work item descriptors
-    int* offsets;               // [n_tiles * 4 + 1]   exclusive prefix of counts
-    int* cursor;                // [n_tiles * 4]       fill position per bin
+    int* offsets;               // [n_bins + 1]        exclusive prefix of counts
+    int* cursor;                // [n_bins]            fill position per bin
     int* tile_chunks;           // [n_tiles + 1]       exclusive prefix of work items per tile
     int* items;                 // [max_items]         work item -> tile
     int* block_sums;            // [2 * scan_blocks]
