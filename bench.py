@@ -87,8 +87,9 @@ def copy_peak_gbs(torch) -> float:
     return 2 * n * 4 / best / 1e9
 
 
-def touched_rows(inp: workloads.Inputs) -> int:
-    """Distinct (n, pixel, head) value rows read by at least one in-range corner.
+def touched_rows(inp: workloads.Inputs):
+    """Distinct (n, pixel, head) value rows read by at least one in-range corner, and the number of
+    in-range samples (each gathers four corner rows).
 
     Uses the same coordinate convention as the operator (fp32 fma, align_corners=False); it only
     sizes the compulsory traffic and takes no part in any result.
@@ -96,6 +97,7 @@ def touched_rows(inp: workloads.Inputs) -> int:
     w = inp.w
     N, Lq, M, L, P = w.N, w.Lq, w.M, w.L, w.P
     keys = []
+    valid = 0
     n_idx = np.arange(N, dtype=np.int64)[:, None, None, None]
     m_idx = np.arange(M, dtype=np.int64)[None, None, :, None]
     for l in range(L):
@@ -107,6 +109,7 @@ def touched_rows(inp: workloads.Inputs) -> int:
         w_im = (x * W - 0.5).astype(np.float32).astype(np.float64)
         h_im = (y * H - 0.5).astype(np.float32).astype(np.float64)
         ok = (h_im > -1) & (w_im > -1) & (h_im < H) & (w_im < W)
+        valid += int(ok.sum())
         h0 = np.floor(h_im).astype(np.int64)
         w0 = np.floor(w_im).astype(np.int64)
         for dh in (0, 1):
@@ -115,7 +118,7 @@ def touched_rows(inp: workloads.Inputs) -> int:
                 v = ok & (hc >= 0) & (hc < H) & (wc >= 0) & (wc < W)
                 row = (n_idx * w.S + st + hc * W + wc) * M + m_idx
                 keys.append(row[v])
-    return int(np.unique(np.concatenate(keys)).size)
+    return int(np.unique(np.concatenate(keys)).size), valid
 
 
 class _Locations:
@@ -134,13 +137,13 @@ def compulsory_bytes(inp, fused: bool = False):
     w = inp.w
     T = w.samples
     es = 2 if w.dtype == "f16" else 4
-    rows = touched_rows(_Locations(inp) if fused else inp)
+    rows, valid = touched_rows(_Locations(inp) if fused else inp)
     touched = rows * w.D * es
     io = w.N * w.Lq * w.M * w.D * es
     ref = w.N * w.Lq * w.L * 8 if fused else 0
     fwd = touched + T * 8 + T * 4 + ref + io
     bwd = touched + T * 8 + T * 4 + ref + io + w.N * w.S * w.M * w.D * 4 + T * 8 + T * 4 + ref
-    return fwd, bwd, rows
+    return fwd, bwd, rows, valid * 4 * w.D * es
 
 
 def cpu_baseline(inp, budget_s: float = 10.0, fused: bool = False):
@@ -316,7 +319,7 @@ def main():
     }
     if not args.no_compulsory:
         print("[bench] counting compulsory bytes", file=sys.stderr, flush=True)
-        fb, bb, rows = compulsory_bytes(inp, args.fused)
+        fb, bb, rows, gathered = compulsory_bytes(inp, args.fused)
         bwd_s = float(bwd_ms.mean()) / 1e3
         fwd_s = float(fwd_ms.mean()) / 1e3
         achieved = bb / bwd_s / 1e9
@@ -331,7 +334,11 @@ def main():
                                "msda_forward (fwd_kernel)",
                                "achieved": round(fb / fwd_s / 1e9, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                                "frac": round(fb / fwd_s / 1e9 / HBM_PEAK_GBS, 5), "algorithmic_bytes": int(fb),
-                               "launch_ms": round(fwd_s * 1e3, 5)}
+                               "launch_ms": round(fwd_s * 1e3, 5),
+                               # the four corner rows of every in-range sample, read through the
+                               # vector memory path (mostly L2 hits): the rate this kernel is bound by
+                               "gathered_bytes": int(gathered),
+                               "gathered_TBps": round(gathered / fwd_s / 1e12, 3)}
         res["step_hbm_frac"] = round((fb + bb) / (step_ms / 1e3) / 1e9 / HBM_PEAK_GBS, 5)
         res["touched_value_rows"] = rows
     if not args.no_cpu_baseline:
