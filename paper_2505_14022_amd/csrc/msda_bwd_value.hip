@@ -723,15 +723,18 @@ __global__ __launch_bounds__(256, 2) void fold_runs_kernel(Params p) {
     const int sub = lane % kLPR, grp = lane / kLPR;  // lane within its record stream, stream
     constexpr int kRecPerLane = kChunkRecords / 64;
 
-    // Work items are dealt from eight queues: queue x holds items x, x + 8, x + 16, ... and serves
-    // the waves of XCD x (workgroups are dispatched to the eight XCDs in turn). The waves in flight
-    // still work on neighbouring items in slab-major order. Each counter has a 256-byte line of its
+    // Work items are dealt from eight queues: queue x holds the x-th eighth of the items (a
+    // contiguous range in slab-major order) and serves the waves of XCD x (workgroups are
+    // dispatched to the eight XCDs in turn), so each XCD's L2 sees the grad_out rows of few slabs
+    // (2-4 us off the backward against dealing items x, x + 8, ...). Each counter has a 256-byte line of its
     // own: all waves taking items from one counter (or from counters sharing a line) serialize on
     // it, which cost the fold a quarter of its time. A wave whose queue has drained helps the others.
     int total = p.tile_chunks[p.n_tiles];
     total = total < 0 ? 0 : (total > p.max_items ? p.max_items : total);
     int owner = blockIdx.x & (kQueues - 1), visited = 0;
-    auto owned = [&](int q) { return (total - q + kQueues - 1) / kQueues; };
+    auto qbase = [&](int q) { return (int)(((int64_t)total * q) / kQueues); };
+    auto owned = [&](int q) { return qbase(q + 1) - qbase(q); };
+    auto item_at = [&](int q, int s) { return qbase(q) + s; };
     auto counter = [&](int q) { return p.queue + q * kQueueStride; };
     // descriptor of work item `it`: lanes 0..15 hold its 16 words
     auto load_desc = [&](int it) { return lane < 16 ? p.item_desc[(size_t)it * 16 + lane] : 0; };
@@ -773,7 +776,7 @@ __global__ __launch_bounds__(256, 2) void fold_runs_kernel(Params p) {
             }
             continue;
         }
-        const int item = slot * kQueues + owner;
+        const int item = item_at(owner, slot);
         // the next slot is taken now; it is needed only when this item is done
         if (lane == 0) taken = atomicAdd(counter(owner), 1);
         const int dv = item == pf_item ? pf_dv : load_desc(item);
@@ -860,7 +863,7 @@ __global__ __launch_bounds__(256, 2) void fold_runs_kernel(Params p) {
         {
             const int nslot = __builtin_amdgcn_readfirstlane(taken);
             if (nslot < owned(owner)) {
-                pf_item = nslot * kQueues + owner;
+                pf_item = item_at(owner, nslot);
                 pf_dv = load_desc(pf_item);
             }
         }
