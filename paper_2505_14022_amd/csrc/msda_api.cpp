@@ -212,6 +212,8 @@ msda_status_t backward_body(const void* value, const int64_t* shapes, const int6
             e = msda::launch_prologue(p, const_cast<float*>(p.loc), const_cast<float*>(p.attn), s);
             if (e != hipSuccess) return fail(MSDA_ERROR_LAUNCH_FAILED, "prologue launch: %s", hipGetErrorString(e));
         }
+        // grad_loc / grad_attn are final outputs unless the prologue's chain rule reads them back
+        p.stream_grads = !pro || (grads_in_kernel && !pro->grad_ref);
         if (grads_in_kernel) {
             const int64_t q0 = n0 * Lq * M * L * P;
             p.prologue_grads = 1;

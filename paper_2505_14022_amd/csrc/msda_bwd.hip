@@ -170,13 +170,21 @@ __global__ __launch_bounds__(kBlock) void bwd_kernel(Params p) {
                 if (p.prologue_grads) {
                     // the offsets are in pixels of the level: d loc / d offset = 1 / (W_l, H_l), which
                     // cancels the level size of grad_loc
-                    reinterpret_cast<float2*>(p.grad_loc)[smp] = make_float2(a * gw, a * gh);
+                    float2* gl = reinterpret_cast<float2*>(p.grad_loc) + smp;
+                    if (p.stream_grads) stream_store(gl, make_float2(a * gw, a * gh));
+                    else *gl = make_float2(a * gw, a * gh);
                     s_x[wave][j] = make_float4(a, ga, a * ga, 0.f);
                 } else {
                     const int l = (k0 + jk) / p.P;
                     const float Wf = (float)s_lvl[kMaxLevels + l], Hf = (float)s_lvl[l];
-                    p.grad_attn[smp] = ga;
-                    reinterpret_cast<float2*>(p.grad_loc)[smp] = make_float2(Wf * (a * gw), Hf * (a * gh));
+                    float2* gl = reinterpret_cast<float2*>(p.grad_loc) + smp;
+                    if (p.stream_grads) {
+                        stream_store(p.grad_attn + smp, ga);
+                        stream_store(gl, make_float2(Wf * (a * gw), Hf * (a * gh)));
+                    } else {
+                        p.grad_attn[smp] = ga;
+                        *gl = make_float2(Wf * (a * gw), Hf * (a * gh));
+                    }
                 }
             }
         }
@@ -193,7 +201,9 @@ __global__ __launch_bounds__(kBlock) void bwd_kernel(Params p) {
                     // the weight itself, also where the sample is off the map (there grad_attn = 0
                     // but the softmax still ties its logit to the others)
                     const int smp = ((t.n * p.Lq + q) * p.M + t.m) * K + k0 + jk;
-                    p.grad_attn[smp] = p.attn[smp] * (s_x[wave][j].y - dot);
+                    const float gz = p.attn[smp] * (s_x[wave][j].y - dot);
+                    if (p.stream_grads) stream_store(p.grad_attn + smp, gz);
+                    else p.grad_attn[smp] = gz;
                 }
             }
         }

@@ -957,7 +957,7 @@ __global__ __launch_bounds__(256, 2) void fold_runs_kernel(Params p) {
                     if (px < TH * TW && r < th_on && c < tw_on && ch0 + 4 * q < D) {
                         float* dst = p.grad_value + ((size_t)(n * p.S + st + (h_org + r) * W + w_org + c) * p.M + m) * D +
                                      ch0 + 4 * q;
-                        *reinterpret_cast<float4*>(dst) = v;
+                        stream_store(reinterpret_cast<float4*>(dst), v);
                     }
                 }
             } else {

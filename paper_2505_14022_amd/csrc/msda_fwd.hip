@@ -102,7 +102,7 @@ __global__ __launch_bounds__(kBlock) void fwd_kernel(Params p) {
             }
         }
         if (active && q_mine < p.Lq)
-            Row<T, VEC>::store(out + ((size_t)(t.n * p.Lq + q_mine) * p.M + t.m) * p.D + chan, acc);
+            Row<T, VEC>::store_final(out + ((size_t)(t.n * p.Lq + q_mine) * p.M + t.m) * p.D + chan, acc);
     }
 }
 

@@ -40,6 +40,7 @@ struct Params {
     float* grad_loc;       // [n_batch, Lq, M, L, P, 2]                      (backward)
     float* grad_attn;      // [n_batch, Lq, M, L, P]                         (backward)
     int prologue_grads;    // backward: grad_loc / grad_attn hold grad_offsets / grad_logits instead
+    int stream_grads;      // backward: grad_loc / grad_attn are read by no later kernel of the call
     uint32_t value_bytes;  // size of the value buffer resource
     uint32_t gv_bytes;     // size of the grad_value buffer resource
     int n_batch, S, M, D, Lq, L, P, K;  // K = L*P samples per (query, head)
