@@ -600,7 +600,8 @@ constexpr int kPixQ = 8;                          // float4 per 32-channel pixel
 constexpr int kLPR = MSDA_FOLD_LANES_PER_RECORD;  // lanes that share one record (32 channels)
 constexpr int kQPL = kPixQ / kLPR;                // float4 of a record's row per lane
 constexpr int kGroups = 64 / kLPR;                // record streams per wave
-constexpr int kRunBatch = 2 * kLPR;               // records in flight per stream (128 rows per wave)
+constexpr int kRunBatch = 2 * kLPR;               // records loaded together per stream (128 rows per wave)
+constexpr int kUnitRunMax = 12;                  // records per run up to which an item is folded by work units
 static_assert(kLPR == 2 || kLPR == 4 || kLPR == 8, "lanes per record");
 constexpr int kQueues = 8;                                 // fold work queues, one per XCD
 constexpr int kQueueStride = 64;                           // ints between queue counters (256 B)
@@ -689,28 +690,35 @@ __device__ __forceinline__ void flush_run(float4* acc, int key, int TH, int TW, 
 //   1. every lane loads kChunkRecords/64 records (all loads in flight together) and keys each by
 //      the tile position of its top-left corner; LDS counters rank the records per key;
 //   2. a scan over the keys gives each key's run start, and the records are placed in key order,
-//      with their coordinates replaced by the fractional parts and their keys stored beside them,
-//      so the per-record work below needs neither floor nor key arithmetic. The next item's
-//      descriptor is loaded at this point, so it has arrived when the item is done;
-//   3. the sorted records are cut into 64/kLPR equal slices, one per stream of kLPR lanes that
-//      share a record (32/kLPR channels per lane). A stream reads each record's grad_out row once
-//      and keeps the current run's four corner sums in registers; when the key changes the run
-//      moves to a second register set, and when a stream finishes a run while that set is full,
-//      every stream adds its waiting run into an LDS tile (one pass over the corners for all of
-//      them: 7 streams per pass at the DETR-encoder shape). A run that ends inside a slice ends in
-//      no other slice, so two streams never add the same key at once. The run a slice ends on may
-//      go on in the next slices: those last runs are added after the slices are done, one link of
-//      each chain of equal keys per round. (Fewer lanes per record spread the per-record work and the run ends
-//      over more streams: 4 lanes took 5 % off the backward against 8.)
+//      with their coordinates replaced by the fractional parts, so the per-record work below needs
+//      neither floor nor key arithmetic. The next item's descriptor is loaded at this point, so it
+//      has arrived when the item is done;
+//   3. the records are summed per key (run) in registers by record streams of kLPR lanes
+//      (32/kLPR channels per lane), and each run's sums are added into an LDS tile once:
+//      * short runs (an item whose runs average at most kUnitRunMax records: sparse levels): each
+//        run is cut into work units of at most kRunBatch records; in rounds, each stream takes one
+//        unit, loads its records' grad_out rows together, sums them and adds the sums. Pieces of
+//        one key in one round add in turns, different keys at once, corner by corner;
+//      * long runs (dense levels): the sorted records are cut into equal slices, one per stream. A
+//        stream keeps its current run's sums in registers; when its key changes the run moves to a
+//        second register set, and when a stream finishes a run while that set is full, every
+//        stream adds its waiting run at once. A run that ends inside a slice ends in no other
+//        slice, so two streams never add the same key at once; the runs the slices end on are
+//        added afterwards in rounds, by their rank among slices ending on the same key.
+//      With only the slices, streams moved a finished run aside nearly every record at sparse
+//      levels (twice the VALU work of the sums); with only the units, dense items added the many
+//      pieces of their few keys in turns: the two forms together took 1-4 % off the backward at the
+//      DETR, Swin and BEV shapes, against slices alone; units alone made the DETR backward 8 % slower.
 //   4. the tile's on-map pixels are stored once (plain stores), or added with atomics when the
 //      tile is split over several work items (its rows were zeroed before).
-// Every grad_out row read past a slice's end uses an out-of-range buffer offset, which returns zeros.
+// Every grad_out row read past a unit's or a slice's end uses an out-of-range buffer offset, which
+// returns zeros.
 template <typename T>
 __global__ __launch_bounds__(256, 2) void fold_runs_kernel(Params p) {
     __shared__ int s_geo[kGeo * kMaxLevels];
     __shared__ int s_start[kAccWaves][kRunKeys + 1];
     __shared__ int4 s_rec[kAccWaves][kChunkRecords];        // sorted records: {grad_out row, a, lh, lw}
-    __shared__ int s_key[kAccWaves][kChunkRecords];         // and their keys
+    __shared__ int s_key[kAccWaves][kChunkRecords];         // their keys, or the work units (step 3)
     __shared__ float4 s_acc[kAccWaves][kRunPix * kPixQ];    // 32 channels of the tile
     load_geo(p, s_geo);
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
@@ -868,83 +876,171 @@ __global__ __launch_bounds__(256, 2) void fold_runs_kernel(Params p) {
             }
         }
 
-        // 3. slices of equal length
+        // 3. The records are summed per key (run) in registers by record streams of kLPR lanes
+        //    (32/kLPR channels per lane), and each run's sums are added into an LDS tile once.
+        //    Short runs (sparse levels): work units of at most kRunBatch records of one key, one unit
+        //    per stream per round. Long runs (dense levels): equal slices of the sorted records, one
+        //    per stream, a run's sums moved aside when the stream's key changes.
         const int C = start[nkeys];
+        int nonempty = 0;
+#pragma unroll
+        for (int j = 0; j < kKeysPerLane; ++j) {
+            const int k = kKeysPerLane * lane + j;
+            nonempty += __builtin_popcountll(__ballot(k < nkeys && start[k + 1] > start[k]));
+        }
+        const bool by_units = C <= kUnitRunMax * nonempty;
+        int nunits = 0;
+        if (by_units) {
+            {
+                int cnt[kKeysPerLane], pcs[kKeysPerLane], sum = 0;
+#pragma unroll
+                for (int j = 0; j < kKeysPerLane; ++j) {
+                    const int k = kKeysPerLane * lane + j;
+                    cnt[j] = k < nkeys ? start[k + 1] - start[k] : 0;
+                    pcs[j] = (cnt[j] + kRunBatch - 1) / kRunBatch;
+                    sum += pcs[j];
+                }
+                int incl = sum;
+                for (int o = 1; o < 64; o <<= 1) {
+                    const int v = __shfl_up(incl, o, 64);
+                    if (lane >= o) incl += v;
+                }
+                nunits = __builtin_amdgcn_readlane(incl, 63);
+                int u = incl - sum;
+#pragma unroll
+                for (int j = 0; j < kKeysPerLane; ++j) {
+                    const int k = kKeysPerLane * lane + j;
+                    for (int pc = 0; pc < pcs[j]; ++pc, ++u) {
+                        const int beg = start[k] + pc * kRunBatch, len = min(kRunBatch, cnt[j] - pc * kRunBatch);
+                        if (u < kChunkRecords) skey[u] = beg | (len << 10) | (k << 14) | (pc << 22);
+                    }
+                }
+            }
+            wave_lds_sync();
+            nunits = min(nunits, kChunkRecords);
+        }
         const int lo = (C * grp) / kGroups, hi = (C * (grp + 1)) / kGroups;
         const int span = (C + kGroups - 1) / kGroups;
-        const int key_lo = hi > lo ? skey[lo] : 0;  // key of the slice's first record
+        const int key_lo = !by_units && hi > lo ? skey[lo] : 0;  // key of the slice's first record
         for (int ch0 = 0; ch0 < D; ch0 += 4 * kPixQ) {
             const int ch = ch0 + 4 * kQPL * sub;  // the lane's first channel
 #pragma unroll
             for (int it = 0; it < kRunPix * kPixQ / 64; ++it) acc[lane + 64 * it] = make_float4(0.f, 0.f, 0.f, 0.f);
             wave_lds_sync();
-            int cur = key_lo, pkey = -1;  // pkey: key of the finished run waiting in `pend`, or -1
-            Corners run = {}, pend = {};
-            for (int b = 0; b < span; b += kRunBatch) {
-                uint32_t off[kRunBatch];
-                float ra[kRunBatch], rh[kRunBatch], rw[kRunBatch];
-                int rk[kRunBatch];
+            if (by_units) {
+                // rounds of kGroups units, one per record stream: a stream sums its unit's records for
+                // the four corners in registers and adds the sums into the LDS tile once
+                for (int u0 = 0; u0 < nunits; u0 += kGroups) {
+                    const int u = u0 + grp;
+                    const int wd = u < nunits ? skey[u] : 0;
+                    const int beg = wd & 1023, len = u < nunits ? (wd >> 10) & 15 : 0;
+                    const int key = (wd >> 14) & 255, pc = (wd >> 22) & 63;
+                    uint32_t off[kRunBatch];
+                    float ra[kRunBatch], rh[kRunBatch], rw[kRunBatch];
 #pragma unroll
-                for (int u = 0; u < kRunBatch; ++u) {
-                    const int pos = lo + b + u;
-                    const bool act = pos < hi;
-                    const int4 e = srec[act ? pos : 0];
-                    rk[u] = skey[act ? pos : 0];
-                    off[u] = act ? (uint32_t)(e.x + ch) : (uint32_t)kOOBElem;
-                    ra[u] = act ? __builtin_bit_cast(float, e.y) : 0.f;
-                    rh[u] = act ? __builtin_bit_cast(float, e.z) : 0.f;
-                    rw[u] = act ? __builtin_bit_cast(float, e.w) : 0.f;
-                }
-                float4 g[kRunBatch][kQPL];
-#pragma unroll
-                for (int u = 0; u < kRunBatch; ++u)
-#pragma unroll
-                    for (int j = 0; j < kQPL; ++j)  // channels past D read zeros (out-of-range offset)
-                        g[u][j] = QuadBuf<T, 4>::load(gr, ch + 4 * j < D ? off[u] + 4 * j : (uint32_t)kOOBElem);
-#pragma unroll
-                for (int u = 0; u < kRunBatch; ++u) {
-                    const int pos = lo + b + u;
-                    const int key = rk[u];
-                    const bool ends = pos < hi && key != cur;  // the run of key `cur` ends here
-                    // A finished run waits in `pend` until some stream finishes another one while
-                    // its own slot is full; then every waiting run is added at once, so one pass
-                    // over the corners serves many streams instead of one.
-                    if (__ballot(ends && pkey >= 0) != 0) {
-                        if (pkey >= 0) flush_run(acc, pkey, TH, TW, sub, pend);
-                        pkey = -1;
+                    for (int v = 0; v < kRunBatch; ++v) {
+                        const bool act = v < len;
+                        const int4 e = srec[act ? beg + v : 0];
+                        off[v] = act ? (uint32_t)(e.x + ch) : (uint32_t)kOOBElem;
+                        ra[v] = act ? __builtin_bit_cast(float, e.y) : 0.f;
+                        rh[v] = act ? __builtin_bit_cast(float, e.z) : 0.f;
+                        rw[v] = act ? __builtin_bit_cast(float, e.w) : 0.f;
                     }
-                    // selects rather than a divergent branch, so that `run` keeps its registers
-                    const uint64_t ended = __ballot(ends);
-                    if (ended != 0) {
-                        park_run(pend, run, ended);
-                        pkey = ends ? cur : pkey;
-                        cur = ends ? key : cur;
+                    float4 g[kRunBatch][kQPL];
+#pragma unroll
+                    for (int v = 0; v < kRunBatch; ++v)
+#pragma unroll
+                        for (int j = 0; j < kQPL; ++j)  // channels past D read zeros (out-of-range offset)
+                            g[v][j] = QuadBuf<T, 4>::load(gr, ch + 4 * j < D ? off[v] + 4 * j : (uint32_t)kOOBElem);
+                    Corners run = {};
+#pragma unroll
+                    for (int v = 0; v < kRunBatch; ++v) {
+                        // records past the unit have a = 0 and zero rows: they add nothing
+                        const float lh = rh[v], lw = rw[v], a = ra[v];
+                        const float ah = a * (1.f - lh), al = a * lh, hw = 1.f - lw;
+                        const float wk[4] = {ah * hw, ah * lw, al * hw, al * lw};
+#pragma unroll
+                        for (int k = 0; k < 4; ++k)
+#pragma unroll
+                            for (int j = 0; j < kQPL; ++j) add4(run.v[k][j], wk[k], g[v][j]);
                     }
-                    // records past the slice have a = 0 and zero rows: they add nothing
-                    const float lh = rh[u], lw = rw[u], a = ra[u];
-                    const float ah = a * (1.f - lh), al = a * lh, hw = 1.f - lw;
-                    const float wk[4] = {ah * hw, ah * lw, al * hw, al * lw};
-#pragma unroll
-                    for (int k = 0; k < 4; ++k)
-#pragma unroll
-                        for (int j = 0; j < kQPL; ++j) add4(run.v[k][j], wk[k], g[u][j]);
+                    // Units of one key are consecutive, so in this round the pieces of a key sit on
+                    // consecutive streams and a stream's rank among them is min(grp, pc). Rank j adds in
+                    // pass j; within a pass the keys differ, so no two streams add the same pixel as the
+                    // same corner, and flush_run takes the corners one after another.
+                    const int rank = len > 0 ? min(grp, pc) : -1;
+                    for (int j = 0; __ballot(rank == j) != 0; ++j)
+                        if (rank == j) flush_run(acc, key, TH, TW, sub, run);
                 }
-            }
-            // the finished runs still waiting (their keys differ: each ended inside its own slice)
-            if (pkey >= 0) flush_run(acc, pkey, TH, TW, sub, pend);
-            // the runs the slices end on: a key may end several neighbouring slices. Each slice
-            // counts the earlier slices that end on its key; round j adds the sums of the slices
-            // with count j, so no two streams add the same key at once
-            const int last = hi > lo ? cur : -1;
-            int link = 0;
+            } else {
+                int cur = key_lo, pkey = -1;  // pkey: key of the finished run waiting in `pend`, or -1
+                Corners run = {}, pend = {};
+                for (int b = 0; b < span; b += kRunBatch) {
+                    uint32_t off[kRunBatch];
+                    float ra[kRunBatch], rh[kRunBatch], rw[kRunBatch];
+                    int rk[kRunBatch];
 #pragma unroll
-            for (int j = 0; j < kGroups; ++j) {
-                const int kj = __builtin_amdgcn_readlane(last, kLPR * j);
-                link += (j < grp && kj == last) ? 1 : 0;
-            }
+                    for (int u = 0; u < kRunBatch; ++u) {
+                        const int pos = lo + b + u;
+                        const bool act = pos < hi;
+                        const int4 e = srec[act ? pos : 0];
+                        rk[u] = skey[act ? pos : 0];
+                        off[u] = act ? (uint32_t)(e.x + ch) : (uint32_t)kOOBElem;
+                        ra[u] = act ? __builtin_bit_cast(float, e.y) : 0.f;
+                        rh[u] = act ? __builtin_bit_cast(float, e.z) : 0.f;
+                        rw[u] = act ? __builtin_bit_cast(float, e.w) : 0.f;
+                    }
+                    float4 g[kRunBatch][kQPL];
+#pragma unroll
+                    for (int u = 0; u < kRunBatch; ++u)
+#pragma unroll
+                        for (int j = 0; j < kQPL; ++j)  // channels past D read zeros (out-of-range offset)
+                            g[u][j] = QuadBuf<T, 4>::load(gr, ch + 4 * j < D ? off[u] + 4 * j : (uint32_t)kOOBElem);
+#pragma unroll
+                    for (int u = 0; u < kRunBatch; ++u) {
+                        const int pos = lo + b + u;
+                        const int key = rk[u];
+                        const bool ends = pos < hi && key != cur;  // the run of key `cur` ends here
+                        // A finished run waits in `pend` until some stream finishes another one while
+                        // its own slot is full; then every waiting run is added at once, so one pass
+                        // over the corners serves many streams instead of one.
+                        if (__ballot(ends && pkey >= 0) != 0) {
+                            if (pkey >= 0) flush_run(acc, pkey, TH, TW, sub, pend);
+                            pkey = -1;
+                        }
+                        // selects rather than a divergent branch, so that `run` keeps its registers
+                        const uint64_t ended = __ballot(ends);
+                        if (ended != 0) {
+                            park_run(pend, run, ended);
+                            pkey = ends ? cur : pkey;
+                            cur = ends ? key : cur;
+                        }
+                        // records past the slice have a = 0 and zero rows: they add nothing
+                        const float lh = rh[u], lw = rw[u], a = ra[u];
+                        const float ah = a * (1.f - lh), al = a * lh, hw = 1.f - lw;
+                        const float wk[4] = {ah * hw, ah * lw, al * hw, al * lw};
+#pragma unroll
+                        for (int k = 0; k < 4; ++k)
+#pragma unroll
+                            for (int j = 0; j < kQPL; ++j) add4(run.v[k][j], wk[k], g[u][j]);
+                    }
+                }
+                // the finished runs still waiting (their keys differ: each ended inside its own slice)
+                if (pkey >= 0) flush_run(acc, pkey, TH, TW, sub, pend);
+                // the runs the slices end on: a key may end several neighbouring slices. Each slice
+                // counts the earlier slices that end on its key; round j adds the sums of the slices
+                // with count j, so no two streams add the same key at once
+                const int last = hi > lo ? cur : -1;
+                int link = 0;
+#pragma unroll
+                for (int j = 0; j < kGroups; ++j) {
+                    const int kj = __builtin_amdgcn_readlane(last, kLPR * j);
+                    link += (j < grp && kj == last) ? 1 : 0;
+                }
 #pragma unroll 1
-            for (int j = 0; j < kGroups; ++j)
-                if (last >= 0 && link == j) flush_run(acc, last, TH, TW, sub, run);
+                for (int j = 0; j < kGroups; ++j)
+                    if (last >= 0 && link == j) flush_run(acc, last, TH, TW, sub, run);
+            }
             wave_lds_sync();
             // 4. store the tile's on-map pixels
             if (!split) {
