@@ -21,6 +21,34 @@ namespace {
 #endif
 constexpr int kBwdU = MSDA_BWD_UNROLL;
 
+
+// Sums each of the four corner dot products over the query's LPP lanes and stores the four totals
+// in place of the sample's (already read) corner offsets.
+template <int LPP>
+__device__ __forceinline__ void store_corner_sums(float (&G)[4], int sub, int4* slot) {
+    if constexpr (LPP == 8) {
+        // Transposed reduction (10 instructions instead of 16): lanes exchange halves of their
+        // values, so that after two steps lane `sub` of a quad holds corner 2 (sub & 1) + (sub >> 1)
+        // summed over the quad; then lanes 0..3 add the other quad's sum (row_shl:4).
+        const bool b0 = sub & 1, b1 = sub & 2;
+        float x0 = b0 ? G[2] : G[0], x1 = b0 ? G[3] : G[1];
+        const float y0 = b0 ? G[0] : G[2], y1 = b0 ? G[1] : G[3];
+        x0 += dpp<0xB1>(y0);  // lane sub ^ 1
+        x1 += dpp<0xB1>(y1);
+        float z = b1 ? x1 : x0;
+        const float w = b1 ? x0 : x1;
+        z += dpp<0x4E>(w);   // lane sub ^ 2
+        z += dpp<0x104>(z);  // lane sub + 4
+        if (sub < 4) reinterpret_cast<float*>(slot)[2 * (sub & 1) + ((sub >> 1) & 1)] = z;
+    } else {
+#pragma unroll
+        for (int c = 0; c < 4; ++c) G[c] = group_sum<LPP>(G[c]);
+        if (sub == 0)
+            *slot = make_int4(__builtin_bit_cast(int, G[0]), __builtin_bit_cast(int, G[1]),
+                              __builtin_bit_cast(int, G[2]), __builtin_bit_cast(int, G[3]));
+    }
+}
+
 template <typename T, int VEC, int LPP, bool ATOMIC>
 __global__ __launch_bounds__(kBlock) void bwd_kernel(Params p) {
     constexpr int PPW = 64 / LPP;
@@ -61,9 +89,33 @@ __global__ __launch_bounds__(kBlock) void bwd_kernel(Params p) {
         }
         wave_lds_sync();
         const int base = ps * kn;
+        const bool general = ATOMIC || !one_pass;
+        if (!general) {
+            // the query's channels are one row piece per lane: no channel loop around the loads
+            // (a second register set with the next sample's rows in flight was slower at the
+            // Swin-feature shape and tied elsewhere)
+            const uint32_t cb = (uint32_t)(sub * VEC) << Row<T, VEC>::kShift;
+            for (int kk = 0; kk < kn; ++kk) {
+                const int4 o = s_off[wave][base + kk];
+                float v[4][VEC];
+                Row<T, VEC>::load(v[0], vr, ((uint32_t)o.x << Row<T, VEC>::kShift) + cb);
+                Row<T, VEC>::load(v[1], vr, ((uint32_t)o.y << Row<T, VEC>::kShift) + cb);
+                Row<T, VEC>::load(v[2], vr, ((uint32_t)o.z << Row<T, VEC>::kShift) + cb);
+                Row<T, VEC>::load(v[3], vr, ((uint32_t)o.w << Row<T, VEC>::kShift) + cb);
+                float G[4];
+#pragma unroll
+                for (int c = 0; c < 4; ++c) {
+                    G[c] = 0.f;
+#pragma unroll
+                    for (int i = 0; i < VEC; ++i) G[c] += g_row[i] * v[c][i];
+                }
+                // the sums overwrite only this sample's (already read) slot
+                store_corner_sums<LPP>(G, sub, &s_off[wave][base + kk]);
+            }
+        }
         // kBwdU samples at a time: their 4 * kBwdU corner rows are loaded together, then the sums
         // over the query's lanes of all of them are formed together
-        for (int kk0 = 0; kk0 < kn; kk0 += kBwdU) {
+        for (int kk0 = 0; general && kk0 < kn; kk0 += kBwdU) {
             int4 off[kBwdU];
             float a[kBwdU], lh[kBwdU], lw[kBwdU];
 #pragma unroll
