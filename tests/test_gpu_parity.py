@@ -69,6 +69,34 @@ def test_many_tiles_multi_pass_scan():
     check_parity(inp, workspace="owner")
 
 
+def _hot_cell_case(n_hot: int, n_spread: int, seed: int):
+    """One 8 x 8 map (one fold tile per slab, one work item): n_hot samples of each slab fall in one
+    pixel cell (one key), the other n_spread are spread over the whole map."""
+    P, Lq = 4, (n_hot + n_spread) // 4
+    inp = workloads.random_case(1, 2, 32, ((8, 8),), P, Lq, "f32", seed=seed)
+    rng = np.random.default_rng(seed)
+    loc = inp.loc.reshape(1, Lq, 2, P, 2)
+    for m in range(2):
+        flat = loc[0, :, m].reshape(-1, 2)  # (q, p) order
+        flat[:] = rng.uniform(0.02, 0.98, size=flat.shape).astype(np.float32)
+        hot = rng.choice(flat.shape[0], size=n_hot, replace=False)
+        # h_im in (3.1, 3.9), w_im in (4.1, 4.9): the cell whose top-left corner is pixel (3, 4)
+        flat[hot, 0] = ((rng.uniform(4.1, 4.9, size=n_hot) + 0.5) / 8).astype(np.float32)
+        flat[hot, 1] = ((rng.uniform(3.1, 3.9, size=n_hot) + 0.5) / 8).astype(np.float32)
+        loc[0, :, m] = flat.reshape(Lq, P, 2)
+    return inp
+
+
+@pytest.mark.parametrize("n_hot,n_spread", [(200, 300), (352, 148), (480, 20)])
+def test_fold_hot_key(n_hot, n_spread):
+    # (200, 300) and (352, 148): runs average under 12 records, so the item is summed by work units,
+    # and the hot key's 25 or 44 pieces fill whole rounds that add in up to 16 passes by rank;
+    # (480, 20): the slice walk, with most slices ending on the hot key
+    inp = _hot_cell_case(n_hot, n_spread, seed=900 + n_hot)
+    say(f"fold hot key: {n_hot} samples in one cell, {n_spread} spread")
+    check_parity(inp, workspace="owner")
+
+
 @pytest.mark.parametrize("lo,hi", [(-0.6, 1.6), (0.0, 1.0), (0.45, 0.55)])
 def test_location_ranges(lo, hi):
     inp = workloads.random_case(2, 4, 32, ((13, 17), (7, 9)), 4, 123, "f32", seed=7, lo=lo, hi=hi)
