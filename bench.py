@@ -181,6 +181,8 @@ def main():
     ap.add_argument("--no-compulsory", action="store_true", help="skip counting touched rows (faster)")
     ap.add_argument("--atomic-grad-value", action="store_true",
                     help="pass no workspace, so msda_backward accumulates grad_value with fp32 atomics")
+    ap.add_argument("--deterministic", action="store_true",
+                    help="time msda_backward_deterministic (bitwise reproducible grad_value) as the backward")
     ap.add_argument("--fused", action="store_true",
                     help="time msda_forward_fused + msda_backward_fused (inputs: reference points, pixel offsets, "
                          "logits)")
@@ -252,7 +254,8 @@ def main():
         loc, attn = dev_in(inp.loc), dev_in(inp.attn)
         gl = torch.empty(tuple(loc.shape), dtype=torch.float32, device=dev)
         ga = torch.empty(tuple(attn.shape), dtype=torch.float32, device=dev)
-        ws_bytes = 0 if args.atomic_grad_value else msda.workspace_size(inp.shapes, inp.starts, *dims, dt)
+        ws_mode = msda.MSDA_WORKSPACE_DETERMINISTIC if args.deterministic else msda.MSDA_WORKSPACE_PREFERRED
+        ws_bytes = 0 if args.atomic_grad_value else msda.workspace_size(inp.shapes, inp.starts, *dims, dt, ws_mode)
         binned_bytes = ws_bytes
         ws = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device=dev)
         P_ = (value.data_ptr(), loc.data_ptr(), attn.data_ptr(), gout.data_ptr(), out.data_ptr(), gv.data_ptr(),
@@ -265,7 +268,7 @@ def main():
 
         def bwd():
             r = msda.backward_raw(P_[0], shapes, starts, P_[1], P_[2], P_[3], P_[5], P_[6], P_[7], P_[8],
-                                  ws_bytes, dims, dt, sp)
+                                  ws_bytes, dims, dt, sp, deterministic=args.deterministic)
             if r:
                 raise msda.MsdaError(r, "msda_backward", msda.last_error())
 
@@ -314,7 +317,8 @@ def main():
         "fwd_ms_median": round(float(np.median(fwd_ms)), 5),
         "bwd_ms_mean": round(float(bwd_ms.mean()), 5),
         "bwd_ms_median": round(float(np.median(bwd_ms)), 5),
-        "grad_value_path": "owner-computes (binned)" if binned_bytes else "atomic",
+        "grad_value_path": ("owner-computes (binned, deterministic)" if args.deterministic else
+                            "owner-computes (binned)") if binned_bytes else "atomic",
         "workspace_bytes": int(ws_bytes),
     }
     if not args.no_compulsory:

@@ -119,11 +119,36 @@ msda_status_t msda_backward(const void* value, const int64_t* spatial_shapes,
                             int64_t N, int64_t S, int64_t M, int64_t D, int64_t Lq, int64_t L,
                             int64_t P, int dtype, void* stream);
 
+/*
+ * Backward pass with a bitwise reproducible grad_value: the same as msda_backward (same arguments,
+ * layouts, ownership and results within rounding), except that every grad_value element is summed
+ * in an order fixed by the inputs alone, so repeated calls on the same inputs give the same bits
+ * (grad_loc and grad_attn are reproducible on every path). The scatter-add of Sec. 4.2 is
+ * computed owner-by-owner: samples are placed in their tile's bins in sample order, sorted per
+ * pixel in load order, and tiles seen by more than one chunk of 512 samples are summed from the
+ * chunks' partial tiles in chunk order; no float atomics are used. It is slower than
+ * msda_backward and needs a larger workspace.
+ *
+ * workspace: DEVICE scratch of at least msda_backward_workspace_size(...,
+ * MSDA_WORKSPACE_DETERMINISTIC, ...) bytes (about 16 bytes per sample plus 256 * D bytes per work
+ * item), 256-byte aligned, owned by the caller; null or smaller is MSDA_ERROR_INVALID_VALUE.
+ * MSDA_ERROR_NOT_SUPPORTED when D is not a multiple of 4 or the problem's index ranges exceed
+ * 2^31 (the size query reports the same). Lq == 0 zeroes grad_value; N == 0 is a no-op.
+ */
+msda_status_t msda_backward_deterministic(const void* value, const int64_t* spatial_shapes,
+                                          const int64_t* level_start_index, const float* sampling_loc,
+                                          const float* attn_weight, const void* grad_out,
+                                          float* grad_value, float* grad_loc, float* grad_attn,
+                                          void* workspace, size_t workspace_bytes, int64_t N, int64_t S,
+                                          int64_t M, int64_t D, int64_t Lq, int64_t L, int64_t P,
+                                          int dtype, void* stream);
+
 /* Modes of msda_backward_workspace_size. */
 #define MSDA_WORKSPACE_PREFERRED 0 /* the workspace the library would use: 0 bytes where fp32 atomics
                                       are expected to be faster (fewer than one sample per two value
                                       rows, or at most 16384 samples)                               */
 #define MSDA_WORKSPACE_OWNER 1     /* the owner-computes workspace whenever that path applies      */
+#define MSDA_WORKSPACE_DETERMINISTIC 2 /* the workspace of msda_backward_deterministic                */
 
 /*
  * Workspace bytes for msda_backward (host-only; checks the problem like msda_check_args; an

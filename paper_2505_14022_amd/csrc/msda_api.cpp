@@ -169,7 +169,7 @@ SideStream* side_stream() {
 msda_status_t backward_body(const void* value, const int64_t* shapes, const int64_t* starts, const void* grad_out,
                             float* grad_value, const Sampling& smp, const Prologue* pro, void* workspace, int64_t N,
                             int64_t S, int64_t M, int64_t D, int64_t Lq, int64_t L, int64_t P, int dtype,
-                            hipStream_t s) {
+                            hipStream_t s, bool deterministic = false) {
     if (!grad_value) return fail(MSDA_ERROR_INVALID_VALUE, "grad_value must be non-null");
     if (!aligned(grad_value, 16)) return fail(MSDA_ERROR_INVALID_VALUE, "misaligned grad_value: 16 bytes needed");
     if (Lq == 0) {
@@ -192,6 +192,7 @@ msda_status_t backward_body(const void* value, const int64_t* shapes, const int6
         const int64_t smp0 = pro ? 0 : n0 * Lq * M * L * P;  // staging holds one chunk
         msda::Params p = base_params(shapes, starts, S, M, D, Lq, L, P);
         p.n_batch = (int)cnt;
+        p.deterministic = deterministic ? 1 : 0;
         p.value = static_cast<const char*>(value) + n0 * S * M * D * es;
         p.loc = smp.loc + smp0 * 2;
         p.attn = smp.attn + smp0;
@@ -306,14 +307,20 @@ msda_status_t msda_backward_workspace_size(const int64_t* spatial_shapes, const 
     *bytes = 0;
     msda_status_t st = check_problem(spatial_shapes, level_start_index, N, S, M, D, Lq, L, P, dtype);
     if (st != MSDA_SUCCESS) return st;
-    if (mode != MSDA_WORKSPACE_PREFERRED && mode != MSDA_WORKSPACE_OWNER)
+    if (mode != MSDA_WORKSPACE_PREFERRED && mode != MSDA_WORKSPACE_OWNER && mode != MSDA_WORKSPACE_DETERMINISTIC)
         return fail(MSDA_ERROR_INVALID_VALUE, "unknown workspace mode %d", mode);
+    const bool det = mode == MSDA_WORKSPACE_DETERMINISTIC;
+    if (det && D % 4 != 0)
+        return fail(MSDA_ERROR_NOT_SUPPORTED, "the deterministic backward needs D to be a multiple of 4 (D = %lld)",
+                    (long long)D);
     if (N * Lq == 0) return ok();
     const int64_t nb = batch_per_launch(S, M, D, Lq, L, P);
     msda::Params p = base_params(spatial_shapes, level_start_index, S, M, D, Lq, L, P);
     p.n_batch = (int)(N < nb ? N : nb);
+    p.deterministic = det ? 1 : 0;
     if (mode == MSDA_WORKSPACE_PREFERRED && msda::prefer_atomic(p)) return ok();
     if (msda::plan_binned(p)) *bytes = msda::binned_workspace_bytes(p);
+    else if (det) return fail(MSDA_ERROR_NOT_SUPPORTED, "the deterministic backward does not apply to this problem");
     return ok();
 }
 
@@ -350,6 +357,37 @@ msda_status_t msda_backward(const void* value, const int64_t* spatial_shapes, co
     Sampling smp = {sampling_loc, attn_weight, grad_loc, grad_attn};
     return backward_body(value, spatial_shapes, level_start_index, grad_out, grad_value, smp, nullptr,
                          binned ? workspace : nullptr, N, S, M, D, Lq, L, P, dtype, (hipStream_t)stream);
+}
+
+msda_status_t msda_backward_deterministic(const void* value, const int64_t* spatial_shapes,
+                                          const int64_t* level_start_index, const float* sampling_loc,
+                                          const float* attn_weight, const void* grad_out, float* grad_value,
+                                          float* grad_loc, float* grad_attn, void* workspace, size_t workspace_bytes,
+                                          int64_t N, int64_t S, int64_t M, int64_t D, int64_t Lq, int64_t L,
+                                          int64_t P, int dtype, void* stream) {
+    msda_status_t st = check_problem(spatial_shapes, level_start_index, N, S, M, D, Lq, L, P, dtype);
+    if (st != MSDA_SUCCESS) return st;
+    size_t need = 0;
+    st = msda_backward_workspace_size(spatial_shapes, level_start_index, N, S, M, D, Lq, L, P, dtype,
+                                      MSDA_WORKSPACE_DETERMINISTIC, &need);
+    if (st != MSDA_SUCCESS) return st;
+    if (N == 0) return ok();
+    if (Lq > 0) {
+        if (!sampling_loc || !attn_weight || !grad_loc || !grad_attn)
+            return fail(MSDA_ERROR_INVALID_VALUE,
+                        "value, sampling_loc, attn_weight, grad_out, grad_loc and grad_attn must be non-null");
+        if (!aligned(sampling_loc, 8) || !aligned(grad_loc, 8) || !aligned(attn_weight, 4) || !aligned(grad_attn, 4))
+            return fail(MSDA_ERROR_INVALID_VALUE,
+                        "misaligned pointer: value and grad_out need 16 bytes, sampling_loc and grad_loc 8, "
+                        "attn_weight and grad_attn 4");
+        if (!workspace || workspace_bytes < need)
+            return fail(MSDA_ERROR_INVALID_VALUE, "the deterministic backward needs a workspace of %zu bytes (got %zu)",
+                        need, workspace ? workspace_bytes : (size_t)0);
+        if (!aligned(workspace, 256)) return fail(MSDA_ERROR_INVALID_VALUE, "workspace must be 256-byte aligned");
+    }
+    Sampling smp = {sampling_loc, attn_weight, grad_loc, grad_attn};
+    return backward_body(value, spatial_shapes, level_start_index, grad_out, grad_value, smp, nullptr,
+                         Lq > 0 ? workspace : nullptr, N, S, M, D, Lq, L, P, dtype, (hipStream_t)stream, true);
 }
 
 msda_status_t msda_forward_fused(const void* value, const int64_t* spatial_shapes, const int64_t* level_start_index,

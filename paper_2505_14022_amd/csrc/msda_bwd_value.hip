@@ -106,6 +106,8 @@ __device__ __forceinline__ int level_of_tile(const int* g, int L, int tin) {
 
 constexpr int kBinRounds = kCountQueries / 256;  // samples per thread in the count / scatter passes
 
+// DET: the workgroup's histogram row goes to chunk_hist (no atomics), for placement in sample order.
+template <bool DET>
 __global__ __launch_bounds__(256) void bin_count_kernel(Params p) {
     extern __shared__ int hist[];  // bins of this slab
     __shared__ int s_geo[kGeo * kMaxLevels];
@@ -139,11 +141,48 @@ __global__ __launch_bounds__(256) void bin_count_kernel(Params p) {
         if (b >= 0) atomicAdd(&hist[b], 1);
     }
     __syncthreads();
-    int* counts = p.counts + (size_t)slab * bps;
-    for (int i = threadIdx.x; i < bps; i += 256) {
-        const int c = hist[i];
-        if (c) atomicAdd(&counts[i], c);
+    if constexpr (DET) {
+        int* row = p.chunk_hist + (size_t)blockIdx.x * bps;
+        for (int i = threadIdx.x; i < bps; i += 256) row[i] = hist[i];
+    } else {
+        int* counts = p.counts + (size_t)slab * bps;
+        for (int i = threadIdx.x; i < bps; i += 256) {
+            const int c = hist[i];
+            if (c) atomicAdd(&counts[i], c);
+        }
     }
+}
+
+// Deterministic path: per (slab, bin), the exclusive prefix of the counting workgroups' counts in
+// workgroup order (in place), and the bin's total.
+__global__ __launch_bounds__(256) void chunk_scan_kernel(Params p) {
+    const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    const int bps = p.bins_per_slab;
+    if (idx >= (int64_t)p.n_slabs * bps) return;
+    const int slab = (int)(idx / bps), bin = (int)(idx - (int64_t)slab * bps);
+    int* col = p.chunk_hist + (size_t)slab * p.chunks * bps + bin;
+    int run = 0;
+    for (int c = 0; c < p.chunks; ++c) {
+        const int v = col[(size_t)c * bps];
+        col[(size_t)c * bps] = run;
+        run += v;
+    }
+    p.counts[idx] = run;
+}
+
+// Lanes of the wave whose `key` (0 <= key < 2^bits) equals this lane's, among the lanes of `live`.
+__device__ __forceinline__ uint64_t peers_of(int key, int bits, uint64_t live) {
+    uint64_t m = live;
+    for (int b = 0; b < bits; ++b) {
+        const bool set = (key >> b) & 1;
+        const uint64_t bal = __ballot(set);
+        m &= set ? bal : ~bal;
+    }
+    return m;
+}
+
+__device__ __forceinline__ uint64_t lanes_below() {
+    return (1ull << (threadIdx.x & 63)) - 1;
 }
 
 // ---------------------------------------------------------------- 2. scan
@@ -353,6 +392,7 @@ __device__ __forceinline__ void prep_tile(const Params& p, const int* s_geo, int
 
 // Records of one workgroup's (slab, chunk of queries): ranks within the workgroup from LDS
 // counters, one global atomic per bin for the workgroup's base, then the record stores.
+template <bool DET>
 __device__ __forceinline__ void scatter_chunk(const Params& p, const int* s_geo, int* hist, int bps) {
     const int slab = blockIdx.x / p.chunks, chunk = blockIdx.x - slab * p.chunks;
     const int n = slab / p.M, m = slab - n * p.M;
@@ -388,16 +428,42 @@ __device__ __forceinline__ void scatter_chunk(const Params& p, const int* s_geo,
         bins[r] = b;
         ranks[r] = 0;
         if (b >= 0) {
-            ranks[r] = atomicAdd(&hist[b], 1);
+            if constexpr (!DET) ranks[r] = atomicAdd(&hist[b], 1);
             rec[r].z = __builtin_bit_cast(int, h_im);
             rec[r].w = __builtin_bit_cast(int, w_im);
         }
     }
-    __syncthreads();
-    int* cursor = p.cursor + (size_t)slab * bps;
-    for (int i = threadIdx.x; i < bps; i += 256) {
-        const int c = hist[i];
-        if (c) hist[i] = atomicAdd(&cursor[i], c);
+    if constexpr (DET) {
+        // ranks in sample order (round, wave, lane): within a wave from the lanes with the same
+        // bin, across the waves of a round in wave order
+        const int bits = 32 - __builtin_clz((unsigned)(bps > 1 ? bps - 1 : 1));
+        const int wave = threadIdx.x >> 6;
+#pragma unroll
+        for (int r = 0; r < kBinRounds; ++r) {
+            const int b = bins[r];
+            const uint64_t peers = peers_of(b < 0 ? 0 : b, bits, __ballot(b >= 0));
+            const int below = __builtin_popcountll(peers & lanes_below());
+            for (int w = 0; w < kBlock / 64; ++w) {
+                __syncthreads();
+                if (wave == w && b >= 0) {
+                    const int old = hist[b];
+                    ranks[r] = old + below;
+                    __builtin_amdgcn_wave_barrier();
+                    if (below == 0) hist[b] = old + __builtin_popcountll(peers);
+                }
+            }
+        }
+        __syncthreads();
+        const int* base = p.chunk_hist + (size_t)blockIdx.x * bps;
+        const int* off = p.offsets + (size_t)slab * bps;
+        for (int i = threadIdx.x; i < bps; i += 256) hist[i] = off[i] + base[i];
+    } else {
+        __syncthreads();
+        int* cursor = p.cursor + (size_t)slab * bps;
+        for (int i = threadIdx.x; i < bps; i += 256) {
+            const int c = hist[i];
+            if (c) hist[i] = atomicAdd(&cursor[i], c);
+        }
     }
     __syncthreads();
     int4* records = reinterpret_cast<int4*>(p.records);
@@ -410,13 +476,14 @@ __device__ __forceinline__ void scatter_chunk(const Params& p, const int* s_geo,
 }
 
 // Workgroups past n_slabs * chunks only prepare work items (below).
+template <bool DET>
 __global__ __launch_bounds__(256) void bin_scatter_kernel(Params p) {
     extern __shared__ int hist[];  // bins of this slab
     __shared__ int s_geo[kGeo * kMaxLevels];
     const int bps = p.bins_per_slab;
     for (int i = threadIdx.x; i < bps; i += 256) hist[i] = 0;
     load_geo(p, s_geo);
-    if (blockIdx.x < p.n_slabs * p.chunks) scatter_chunk(p, s_geo, hist, bps);
+    if (blockIdx.x < p.n_slabs * p.chunks) scatter_chunk<DET>(p, s_geo, hist, bps);
     // descriptors of the fold's work items (and zeroed rows of split tiles), a few tiles per wave
     for (int t = blockIdx.x * 4 + (threadIdx.x >> 6); t < p.n_tiles; t += gridDim.x * 4)
         prep_tile(p, s_geo, t, threadIdx.x & 63);
@@ -713,7 +780,9 @@ __device__ __forceinline__ void flush_run(float4* acc, int key, int TH, int TW, 
 //      tile is split over several work items (its rows were zeroed before).
 // Every grad_out row read past a unit's or a slice's end uses an out-of-range buffer offset, which
 // returns zeros.
-template <typename T>
+// DET: records ranked per key in load order (ballots instead of LDS atomics), and split tiles'
+// sums written to p.partials for split_reduce_kernel instead of added with atomics.
+template <typename T, bool DET>
 __global__ __launch_bounds__(256, 2) void fold_runs_kernel(Params p) {
     __shared__ int s_geo[kGeo * kMaxLevels];
     __shared__ int s_start[kAccWaves][kRunKeys + 1];
@@ -822,10 +891,25 @@ __global__ __launch_bounds__(256, 2) void fold_runs_kernel(Params p) {
                 const int r = (int)hf - h_org, c = (int)wf - w_org;
                 if (r >= -1 && r < TH && c >= -1 && c < TW) {  // always true for a visible record
                     key[i] = ((r + 1) << kKeyShift) + c + 1;
-                    rank[i] = atomicAdd(&start[key[i]], 1);
+                    if constexpr (!DET) rank[i] = atomicAdd(&start[key[i]], 1);
                     rc[i].z = __builtin_bit_cast(int, __builtin_bit_cast(float, rc[i].z) - hf);
                     rc[i].w = __builtin_bit_cast(int, __builtin_bit_cast(float, rc[i].w) - wf);
                 }
+            }
+        }
+        if constexpr (DET) {
+            // ranks per key in load order (i, lane)
+#pragma unroll
+            for (int i = 0; i < kRecPerLane; ++i) {
+                const uint64_t peers = peers_of(key[i] < 0 ? 0 : key[i], 8, __ballot(key[i] >= 0));
+                const int below = __builtin_popcountll(peers & lanes_below());
+                if (key[i] >= 0) {
+                    const int old = start[key[i]];
+                    rank[i] = old + below;
+                    __builtin_amdgcn_wave_barrier();
+                    if (below == 0) start[key[i]] = old + __builtin_popcountll(peers);
+                }
+                wave_lds_sync();
             }
         }
         wave_lds_sync();
@@ -1056,6 +1140,15 @@ __global__ __launch_bounds__(256, 2) void fold_runs_kernel(Params p) {
                         stream_store(reinterpret_cast<float4*>(dst), v);
                     }
                 }
+            } else if constexpr (DET) {
+                // the item's sums for split_reduce_kernel, every pixel of the tile
+                float4* part = reinterpret_cast<float4*>(p.partials + (size_t)item * kRunPix * D);
+#pragma unroll 4
+                for (int it = 0; it < kRunPix * kPixQ / 64; ++it) {
+                    const int e = lane + 64 * it;
+                    const int px = e / kPixQ, q = e - px * kPixQ;
+                    if (ch0 + 4 * q < D) part[(px * D + ch0 + 4 * q) / 4] = acc[e];
+                }
             } else {
                 // one channel per lane: the atomics of a wave cover whole rows
                 const float* accf = reinterpret_cast<const float*>(acc);
@@ -1079,6 +1172,36 @@ __global__ __launch_bounds__(256, 2) void fold_runs_kernel(Params p) {
 }
 
 }  // namespace
+
+// Deterministic path: grad_value rows of tiles folded by several work items, as the sum of the
+// items' partial tiles in item order (one wave per tile, one channel of a pixel per lane).
+__global__ __launch_bounds__(256) void split_reduce_kernel(Params p) {
+    __shared__ int s_geo[kGeo * kMaxLevels];
+    load_geo(p, s_geo);
+    const int t = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
+    if (t >= p.n_tiles) return;
+    const int first = p.tile_chunks[t];
+    const int nit = min(p.tile_chunks[t + 1], p.max_items) - first;
+    if (nit <= 1) return;
+    const int slab = t / p.tiles_per_slab, tin = t - slab * p.tiles_per_slab;
+    const int n = slab / p.M, m = slab - n * p.M;
+    const int l = level_of_tile(s_geo, p.L, tin);
+    const int H = s_geo[l], W = s_geo[kMaxLevels + l];
+    const int th = s_geo[2 * kMaxLevels + l], tw = s_geo[3 * kMaxLevels + l];
+    const int rel = tin - s_geo[5 * kMaxLevels + l], txn = s_geo[4 * kMaxLevels + l];
+    const int ty = rel / txn, tx = rel - ty * txn;
+    const int st = s_geo[6 * kMaxLevels + l];
+    const int h_org = ty << th, w_org = tx << tw;
+    const int D = p.D;
+    for (int e = lane; e < kRunPix * D; e += 64) {
+        const int px = e / D, ch = e - px * D;
+        const int h = h_org + (px >> tw), w = w_org + (px & ((1 << tw) - 1));
+        if (px >= (1 << (th + tw)) || h >= H || w >= W) continue;
+        float v = 0.f;
+        for (int k = 0; k < nit; ++k) v += p.partials[(size_t)(first + k) * kRunPix * D + e];
+        p.grad_value[((size_t)(n * p.S + st + h * W + w) * p.M + m) * D + ch] = v;
+    }
+}
 
 // ---------------------------------------------------------------- host side
 
@@ -1231,12 +1354,24 @@ int queue_grid() {
 // count of finished workgroups, each counter on a 256-byte line of its own.
 size_t zeroed_ints(const Params& p) { return (size_t)p.n_bins + (kQueues + 1) * kQueueStride; }
 
+// Workgroups of the counting / scatter passes per slab.
+int count_chunks(const Params& p) {
+    const int qpb = kCountQueries / p.K > 0 ? kCountQueries / p.K : 1;
+    return (p.Lq + qpb - 1) / qpb;
+}
+
+size_t deterministic_extra_bytes(const Params& p) {
+    if (!p.deterministic) return 0;
+    return align256((size_t)p.n_slabs * count_chunks(p) * p.bins_per_slab * 4) +
+           align256((size_t)p.max_items * kRunPix * p.D * 4);
+}
+
 size_t binned_workspace_bytes(const Params& p) {
     const size_t nb = (size_t)p.n_bins;
     return align256(zeroed_ints(p) * 4) + align256((size_t)p.max_items * 64) + align256((nb + 1) * 4) + align256(nb * 4) +
            align256(((size_t)p.n_tiles + 1) * 4) +
            align256((size_t)p.max_items * 4) + align256((size_t)p.scan_blocks * 2 * 4) +
-           align256((size_t)p.n_samples * 16);
+           align256((size_t)p.n_samples * 16) + deterministic_extra_bytes(p);
 }
 
 void bind_workspace(Params& p, void* ws) {
@@ -1259,6 +1394,14 @@ void bind_workspace(Params& p, void* ws) {
     p.block_sums = reinterpret_cast<int*>(c);
     c += align256((size_t)p.scan_blocks * 2 * 4);
     p.records = reinterpret_cast<int*>(c);
+    c += align256((size_t)p.n_samples * 16);
+    p.chunk_hist = nullptr;
+    p.partials = nullptr;
+    if (p.deterministic) {
+        p.chunk_hist = reinterpret_cast<int*>(c);
+        c += align256((size_t)p.n_slabs * count_chunks(p) * p.bins_per_slab * 4);
+        p.partials = reinterpret_cast<float*>(c);
+    }
 }
 
 hipError_t launch_binned_reset(const Params& p, hipStream_t stream) {
@@ -1272,7 +1415,16 @@ hipError_t launch_backward_value_binned(const Params& p0, msda_dtype_t dtype, hi
     p.chunks = (p.Lq + p.q_per_block - 1) / p.q_per_block;
     const int bin_blocks = p.n_slabs * p.chunks;
     const size_t hist_lds = (size_t)p.bins_per_slab * sizeof(int);
-    hipLaunchKernelGGL(bin_count_kernel, dim3(bin_blocks), dim3(256), hist_lds, stream, p);
+    const bool det = p.deterministic != 0;
+    if (det && p.D % 4 != 0) return hipErrorNotSupported;
+    if (det) {
+        hipLaunchKernelGGL(bin_count_kernel<true>, dim3(bin_blocks), dim3(256), hist_lds, stream, p);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+        const int64_t cols = (int64_t)p.n_slabs * p.bins_per_slab;
+        hipLaunchKernelGGL(chunk_scan_kernel, dim3((unsigned)((cols + 255) / 256)), dim3(256), 0, stream, p);
+    } else {
+        hipLaunchKernelGGL(bin_count_kernel<false>, dim3(bin_blocks), dim3(256), hist_lds, stream, p);
+    }
     if ((e = hipGetLastError()) != hipSuccess) return e;
     hipLaunchKernelGGL(scan_reduce_kernel, dim3(p.scan_blocks), dim3(256), 0, stream, p);
     if ((e = hipGetLastError()) != hipSuccess) return e;
@@ -1280,16 +1432,25 @@ hipError_t launch_backward_value_binned(const Params& p0, msda_dtype_t dtype, hi
     if ((e = hipGetLastError()) != hipSuccess) return e;
     // the scatter's workgroups also prepare the work items, at least one wave per four tiles
     const int prep_blocks = (p.n_tiles + 15) / 16;
-    hipLaunchKernelGGL(bin_scatter_kernel, dim3(bin_blocks > prep_blocks ? bin_blocks : prep_blocks), dim3(256),
-                       hist_lds, stream, p);
+    const dim3 scatter_grid(bin_blocks > prep_blocks ? bin_blocks : prep_blocks);
+    if (det) hipLaunchKernelGGL(bin_scatter_kernel<true>, scatter_grid, dim3(256), hist_lds, stream, p);
+    else hipLaunchKernelGGL(bin_scatter_kernel<false>, scatter_grid, dim3(256), hist_lds, stream, p);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     if (p.D % 4 == 0) {
         const int grid = queue_grid();  // the waves take work items from the queue
         if (grid <= 0) return hipErrorInvalidConfiguration;
-        if (dtype == MSDA_F16)
-            hipLaunchKernelGGL(fold_runs_kernel<_Float16>, dim3(grid), dim3(256), 0, stream, p);
-        else
-            hipLaunchKernelGGL(fold_runs_kernel<float>, dim3(grid), dim3(256), 0, stream, p);
+        if (det) {
+            if (dtype == MSDA_F16)
+                hipLaunchKernelGGL((fold_runs_kernel<_Float16, true>), dim3(grid), dim3(256), 0, stream, p);
+            else
+                hipLaunchKernelGGL((fold_runs_kernel<float, true>), dim3(grid), dim3(256), 0, stream, p);
+            if ((e = hipGetLastError()) != hipSuccess) return e;
+            hipLaunchKernelGGL(split_reduce_kernel, dim3((unsigned)((p.n_tiles + 3) / 4)), dim3(256), 0, stream, p);
+        } else if (dtype == MSDA_F16) {
+            hipLaunchKernelGGL((fold_runs_kernel<_Float16, false>), dim3(grid), dim3(256), 0, stream, p);
+        } else {
+            hipLaunchKernelGGL((fold_runs_kernel<float, false>), dim3(grid), dim3(256), 0, stream, p);
+        }
         return hipGetLastError();
     }
     int tile_floats = 0;

@@ -64,6 +64,7 @@ struct Params {
     int n_samples;              // n_batch * Lq * M * K
     int max_items;              // capacity of `items`
     int scan_blocks;            // ceil(n_tiles / kScanTiles)
+    int deterministic;          // grad_value summed in an order fixed by the inputs (bitwise reproducible)
     int* counts;                // [n_bins]            samples per bin (tile, class)
     int* queue;                 // [8 * 64]            fold work queue counters, 256 B apart (zeroed with counts)
     int* scan_done;             // [1]                 workgroups of the scan's first pass done (zeroed with counts)
@@ -74,6 +75,9 @@ struct Params {
     int* items;                 // [max_items]         work item -> tile
     int* block_sums;            // [2 * scan_blocks]
     int* records;               // [n_samples][4]      {grad_out row, a, h_im, w_im} per sample, sorted by bin
+    int* chunk_hist;            // [n_slabs * chunks][bins_per_slab] (deterministic) records per counting
+                                //                     workgroup and bin, then their prefix over workgroups
+    float* partials;            // [max_items][64][D]  (deterministic) sums of the work items of split tiles
 };
 
 hipError_t launch_forward(const Params& p, msda_dtype_t dtype, hipStream_t stream);

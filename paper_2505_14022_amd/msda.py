@@ -24,8 +24,10 @@ MSDA_F16 = 1
 MSDA_MAX_LEVELS = 16
 MSDA_WORKSPACE_PREFERRED = 0
 MSDA_WORKSPACE_OWNER = 1
+MSDA_WORKSPACE_DETERMINISTIC = 2
 
-EXPORTED = ["msda_check_args", "msda_forward", "msda_backward", "msda_backward_workspace_size",
+EXPORTED = ["msda_check_args", "msda_forward", "msda_backward", "msda_backward_deterministic",
+            "msda_backward_workspace_size",
             "msda_forward_fused", "msda_backward_fused_workspace_size", "msda_backward_fused",
             "msda_status_string", "msda_last_error", "msda_version"]
 
@@ -54,6 +56,8 @@ def lib():
         L.msda_backward.argtypes = [vp, ip, ip, vp, vp, vp, vp, vp, vp, vp, ctypes.c_size_t] + [i64] * 7 + \
             [ctypes.c_int, vp]
         L.msda_backward.restype = ctypes.c_int
+        L.msda_backward_deterministic.argtypes = L.msda_backward.argtypes
+        L.msda_backward_deterministic.restype = ctypes.c_int
         L.msda_backward_workspace_size.argtypes = [ip, ip] + [i64] * 7 + [ctypes.c_int, ctypes.c_int,
                                                                          ctypes.POINTER(ctypes.c_size_t)]
         L.msda_backward_workspace_size.restype = ctypes.c_int
@@ -204,6 +208,35 @@ def backward(value, spatial_shapes, level_start_index, sampling_loc, attn_weight
     return grad_value, grad_loc, grad_attn
 
 
+def backward_deterministic(value, spatial_shapes, level_start_index, sampling_loc, attn_weight, grad_out,
+                           grad_value=None, grad_loc=None, grad_attn=None, workspace=None, stream=None):
+    """(grad_value fp32, grad_loc, grad_attn) from msda_backward_deterministic (bitwise reproducible
+    grad_value). workspace: a caller-owned uint8 device tensor, or None to allocate one of the size
+    msda_backward_workspace_size(..., MSDA_WORKSPACE_DETERMINISTIC) reports."""
+    import torch
+
+    N, S, M, D, Lq, L, P = _dims(value, sampling_loc)
+    dev = value.device
+    if grad_value is None:
+        grad_value = torch.empty((N, S, M, D), dtype=torch.float32, device=dev)
+    if grad_loc is None:
+        grad_loc = torch.empty(tuple(sampling_loc.shape), dtype=torch.float32, device=dev)
+    if grad_attn is None:
+        grad_attn = torch.empty(tuple(attn_weight.shape), dtype=torch.float32, device=dev)
+    sh, st = _host_tables(spatial_shapes, level_start_index)
+    if workspace is None:
+        nbytes = workspace_size(sh.reshape(-1, 2), st, N, S, M, D, Lq, L, P, _dtype_code(value),
+                                MSDA_WORKSPACE_DETERMINISTIC)
+        workspace = torch.empty(max(nbytes, 1), dtype=torch.uint8, device=dev)
+    ws_bytes = workspace.numel() * workspace.element_size()
+    r = lib().msda_backward_deterministic(_dptr(value), _iptr(sh), _iptr(st), _dptr(sampling_loc),
+                                          _dptr(attn_weight), _dptr(grad_out), _dptr(grad_value), _dptr(grad_loc),
+                                          _dptr(grad_attn), _dptr(workspace), ws_bytes, N, S, M, D, Lq, L, P,
+                                          _dtype_code(value), _stream(stream))
+    _raise(r, "msda_backward_deterministic")
+    return grad_value, grad_loc, grad_attn
+
+
 def _fused_dims(value, ref_points, offsets, logits):
     N, S, M, D = value.shape
     if offsets.dim() != 6 or offsets.shape[-1] != 2:
@@ -290,10 +323,12 @@ def forward_raw(value_ptr: int, shapes: np.ndarray, starts: np.ndarray, loc_ptr:
 
 def backward_raw(value_ptr: int, shapes: np.ndarray, starts: np.ndarray, loc_ptr: int, attn_ptr: int,
                  gout_ptr: int, gv_ptr: int, gl_ptr: int, ga_ptr: int, ws_ptr: Optional[int], ws_bytes: int,
-                 dims: Sequence[int], dtype: int, stream: int) -> int:
-    """msda_backward on raw device addresses; returns the status (used by the benchmark loop)."""
-    return lib().msda_backward(value_ptr, _iptr(shapes), _iptr(starts), loc_ptr, attn_ptr, gout_ptr,
-                               gv_ptr, gl_ptr, ga_ptr, ws_ptr, ws_bytes, *dims, dtype, stream)
+                 dims: Sequence[int], dtype: int, stream: int, deterministic: bool = False) -> int:
+    """msda_backward (or msda_backward_deterministic) on raw device addresses; returns the status
+    (used by the benchmark loop)."""
+    fn = lib().msda_backward_deterministic if deterministic else lib().msda_backward
+    return fn(value_ptr, _iptr(shapes), _iptr(starts), loc_ptr, attn_ptr, gout_ptr, gv_ptr, gl_ptr, ga_ptr, ws_ptr,
+              ws_bytes, *dims, dtype, stream)
 
 
 def forward_fused_raw(value_ptr: int, shapes: np.ndarray, starts: np.ndarray, ref_ptr: int, off_ptr: int,

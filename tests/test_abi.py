@@ -175,6 +175,35 @@ def test_workspace_sizes(L, w):
     assert msda.workspace_size(*_args(w)) == (0 if sparse else owner)
 
 
+@pytest.mark.parametrize("w", workloads.WORKLOADS, ids=lambda w: w.name)
+def test_deterministic_workspace_sizes(L, w):
+    owner = msda.workspace_size(*_args(w), msda.MSDA_WORKSPACE_OWNER)
+    det = msda.workspace_size(*_args(w), msda.MSDA_WORKSPACE_DETERMINISTIC)
+    # the owner-computes workspace plus the counting workgroups' histograms and one 64-pixel partial
+    # tile per work item
+    assert det > owner > 0
+
+
+def test_deterministic_backward_checks(L):
+    a = base()
+    a[5] = 6  # D % 4 != 0: not supported, reported by the size query and by the entry point
+    with pytest.raises(msda.MsdaError) as e:
+        msda.workspace_size(a[0], a[1], *a[2:9], a[9], msda.MSDA_WORKSPACE_DETERMINISTIC)
+    assert e.value.status == msda.MSDA_ERROR_NOT_SUPPORTED
+    ip = ctypes.POINTER(ctypes.c_int64)
+    r = L.msda_backward_deterministic(0x1000, a[0].ctypes.data_as(ip), a[1].ctypes.data_as(ip), 0x2000, 0x3000,
+                                      0x4000, 0x5000, 0x6000, 0x7000, 0x8000, 1 << 30, *a[2:9], a[9], None)
+    assert r == msda.MSDA_ERROR_NOT_SUPPORTED
+    a = base()
+    need = msda.workspace_size(a[0], a[1], *a[2:9], a[9], msda.MSDA_WORKSPACE_DETERMINISTIC)
+    assert need > 0
+    # a null or short workspace is an error, found before anything is launched
+    for ws, nbytes in ((None, 0), (0x8000, need - 1)):
+        r = L.msda_backward_deterministic(0x1000, a[0].ctypes.data_as(ip), a[1].ctypes.data_as(ip), 0x2000,
+                                          0x3000, 0x4000, 0x5000, 0x6000, 0x7000, ws, nbytes, *a[2:9], a[9], None)
+        assert r == msda.MSDA_ERROR_INVALID_VALUE and "workspace" in msda.last_error()
+
+
 def test_workspace_size_not_applicable(L):
     a = base()
     a[5] = 3001  # D % 4 != 0 and D > 355: grad_value by atomics, no workspace

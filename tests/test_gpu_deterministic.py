@@ -1,0 +1,100 @@
+"""GPU tests of msda_backward_deterministic: parity with the oracle, and bit-identical grad_value
+from repeated calls (also after other work has changed what the caches and queues hold)."""
+import numpy as np
+import pytest
+
+from paper_2505_14022_amd import msda, workloads
+from gpu_util import check_parity, require_gpu, run_oracle, say, to_device
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def gpu():
+    require_gpu()
+
+
+def run_det(inp, d=None):
+    import torch
+
+    d = d or to_device(inp)
+    out = msda.forward(d.value, inp.shapes, inp.starts, d.loc, d.attn)
+    gv, gl, ga = msda.backward_deterministic(d.value, inp.shapes, inp.starts, d.loc, d.attn, d.grad_out)
+    torch.cuda.synchronize()
+    return {"out": out.cpu().numpy(), "grad_value": gv.cpu().numpy(), "grad_loc": gl.cpu().numpy(),
+            "grad_attn": ga.cpu().numpy()}
+
+
+SMALL = [
+    # N, M, D, shapes, P, Lq, dtype
+    (1, 2, 8, ((8, 8), (4, 4)), 2, 16, "f32"),
+    (2, 2, 12, ((6, 10), (3, 5), (2, 2)), 2, 33, "f16"),
+    (3, 8, 32, ((20, 30), (10, 15), (5, 8), (3, 4)), 4, 257, "f32"),
+    (3, 8, 32, ((20, 30), (10, 15), (5, 8), (3, 4)), 4, 257, "f16"),
+    (1, 1, 64, ((11, 7), (6, 4)), 8, 101, "f32"),
+    (2, 8, 32, ((16, 24), (8, 12), (4, 6), (2, 3)), 8, 150, "f32"),
+    (1, 2, 260 - 4, ((5, 6), (3, 3)), 2, 19, "f32"),
+]
+
+
+@pytest.mark.parametrize("case", SMALL, ids=lambda c: f"N{c[0]}M{c[1]}D{c[2]}L{len(c[3])}P{c[4]}Lq{c[5]}{c[6]}")
+def test_small_parity(case):
+    N, M, D, shapes, P, Lq, dt = case
+    inp = workloads.random_case(N, M, D, shapes, P, Lq, dt, seed=3000 + D + Lq)
+    say(f"deterministic small case {inp.w.name}")
+    check_parity(inp, gpu=run_det(inp))
+
+
+@pytest.mark.parametrize("seed", range(2))
+def test_split_tiles_parity_and_bits(seed):
+    # dense coarse maps: tiles split over several work items, summed from partial tiles
+    inp = workloads.random_case(2, 4, 32, ((12, 10), (3, 5), (1, 2)), 8, 3000, "f32", seed=60 + seed,
+                                lo=0.2, hi=0.6)
+    say(f"deterministic split tiles seed {seed}")
+    d = to_device(inp)
+    a = run_det(inp, d)
+    check_parity(inp, gpu=a)
+    b = run_det(inp, d)
+    assert np.array_equal(a["grad_value"].view(np.uint32), b["grad_value"].view(np.uint32))
+
+
+@pytest.mark.parametrize("name", ["detr_encoder", "bev_tsa_f16"])
+def test_full_size_bitwise_reproducible(name):
+    import torch
+
+    w = workloads.BY_NAME[name]
+    say(f"deterministic full-size {name}")
+    inp = workloads.generate(w)
+    d = to_device(inp)
+    first = run_det(inp, d)
+    check_parity(inp, gpu=first)
+    # other work in between: the default backward (atomics on split tiles, records in arrival order)
+    # and a side stream, then the deterministic backward again, twice
+    msda.backward(d.value, inp.shapes, inp.starts, d.loc, d.attn, d.grad_out)
+    s = torch.cuda.Stream()
+    with torch.cuda.stream(s):
+        gv, _, _ = msda.backward_deterministic(d.value, inp.shapes, inp.starts, d.loc, d.attn, d.grad_out, stream=s)
+    s.synchronize()
+    again = run_det(inp, d)
+    for k in ("grad_value", "grad_loc", "grad_attn"):
+        assert np.array_equal(first[k].view(np.uint32), again[k].view(np.uint32)), f"{name}: {k} bits differ"
+    assert np.array_equal(first["grad_value"].view(np.uint32), gv.cpu().numpy().view(np.uint32))
+
+
+def test_empty_and_hot_key():
+    import torch
+
+    inp = workloads.random_case(1, 2, 32, ((8, 8),), 4, 0, "f32", seed=5)
+    d = to_device(inp)
+    gv = torch.full(tuple(inp.value.shape), 3.0, device="cuda")
+    msda.backward_deterministic(d.value, inp.shapes, inp.starts, d.loc, d.attn, d.grad_out, grad_value=gv)
+    torch.cuda.synchronize()
+    assert torch.all(gv == 0).item()
+    # one pixel cell takes most samples: the work-unit fold with many pieces of one key per round
+    from test_gpu_parity import _hot_cell_case
+
+    inp = _hot_cell_case(352, 148, seed=77)
+    say("deterministic hot key")
+    check_parity(inp, gpu=run_det(inp))
+    ref = run_oracle(inp)
+    assert ref["grad_value"].shape == inp.value.shape
