@@ -162,10 +162,17 @@ __global__ __launch_bounds__(256) void chunk_scan_kernel(Params p) {
     const int slab = (int)(idx / bps), bin = (int)(idx - (int64_t)slab * bps);
     int* col = p.chunk_hist + (size_t)slab * p.chunks * bps + bin;
     int run = 0;
-    for (int c = 0; c < p.chunks; ++c) {
-        const int v = col[(size_t)c * bps];
-        col[(size_t)c * bps] = run;
-        run += v;
+    // 32 loads in flight at a time: the Swin-feature shape has 428 counting workgroups per slab
+    constexpr int kBatch = 32;
+    for (int c0 = 0; c0 < p.chunks; c0 += kBatch) {
+        int v[kBatch];
+#pragma unroll
+        for (int u = 0; u < kBatch; ++u) v[u] = c0 + u < p.chunks ? col[(size_t)(c0 + u) * bps] : 0;
+#pragma unroll
+        for (int u = 0; u < kBatch; ++u) {
+            if (c0 + u < p.chunks) col[(size_t)(c0 + u) * bps] = run;
+            run += v[u];
+        }
     }
     p.counts[idx] = run;
 }
@@ -434,22 +441,27 @@ __device__ __forceinline__ void scatter_chunk(const Params& p, const int* s_geo,
         }
     }
     if constexpr (DET) {
-        // ranks in sample order (round, wave, lane): within a wave from the lanes with the same
-        // bin, across the waves of a round in wave order
+        // ranks in a fixed order of the workgroup's samples, (wave, round, lane): the waves take
+        // turns, and within a wave's round the lanes with the same bin are ranked by lane
         const int bits = 32 - __builtin_clz((unsigned)(bps > 1 ? bps - 1 : 1));
         const int wave = threadIdx.x >> 6;
+        uint64_t peers[kBinRounds];
 #pragma unroll
-        for (int r = 0; r < kBinRounds; ++r) {
-            const int b = bins[r];
-            const uint64_t peers = peers_of(b < 0 ? 0 : b, bits, __ballot(b >= 0));
-            const int below = __builtin_popcountll(peers & lanes_below());
-            for (int w = 0; w < kBlock / 64; ++w) {
-                __syncthreads();
-                if (wave == w && b >= 0) {
-                    const int old = hist[b];
-                    ranks[r] = old + below;
-                    __builtin_amdgcn_wave_barrier();
-                    if (below == 0) hist[b] = old + __builtin_popcountll(peers);
+        for (int r = 0; r < kBinRounds; ++r) peers[r] = peers_of(bins[r] < 0 ? 0 : bins[r], bits, __ballot(bins[r] >= 0));
+        for (int w = 0; w < kBlock / 64; ++w) {
+            __syncthreads();
+            if (wave == w) {
+#pragma unroll
+                for (int r = 0; r < kBinRounds; ++r) {
+                    const int b = bins[r];
+                    const int below = __builtin_popcountll(peers[r] & lanes_below());
+                    if (b >= 0) {
+                        const int old = hist[b];
+                        ranks[r] = old + below;
+                        __builtin_amdgcn_wave_barrier();
+                        if (below == 0) hist[b] = old + __builtin_popcountll(peers[r]);
+                    }
+                    wave_lds_sync();
                 }
             }
         }
@@ -1174,11 +1186,12 @@ __global__ __launch_bounds__(256, 2) void fold_runs_kernel(Params p) {
 }  // namespace
 
 // Deterministic path: grad_value rows of tiles folded by several work items, as the sum of the
-// items' partial tiles in item order (one wave per tile, one channel of a pixel per lane).
+// items' partial tiles in item order. One workgroup per tile, one element (pixel, channel) per
+// thread and pass; the items' partials are loaded kBatch at a time and added in item order.
 __global__ __launch_bounds__(256) void split_reduce_kernel(Params p) {
     __shared__ int s_geo[kGeo * kMaxLevels];
     load_geo(p, s_geo);
-    const int t = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
+    const int t = blockIdx.x;
     if (t >= p.n_tiles) return;
     const int first = p.tile_chunks[t];
     const int nit = min(p.tile_chunks[t + 1], p.max_items) - first;
@@ -1193,12 +1206,21 @@ __global__ __launch_bounds__(256) void split_reduce_kernel(Params p) {
     const int st = s_geo[6 * kMaxLevels + l];
     const int h_org = ty << th, w_org = tx << tw;
     const int D = p.D;
-    for (int e = lane; e < kRunPix * D; e += 64) {
+    const size_t stride = (size_t)kRunPix * D;  // floats per item
+    for (int e = threadIdx.x; e < kRunPix * D; e += 256) {
         const int px = e / D, ch = e - px * D;
         const int h = h_org + (px >> tw), w = w_org + (px & ((1 << tw) - 1));
         if (px >= (1 << (th + tw)) || h >= H || w >= W) continue;
+        const float* src = p.partials + (size_t)first * stride + e;
         float v = 0.f;
-        for (int k = 0; k < nit; ++k) v += p.partials[(size_t)(first + k) * kRunPix * D + e];
+        constexpr int kBatch = 16;
+        for (int k0 = 0; k0 < nit; k0 += kBatch) {
+            float x[kBatch];
+#pragma unroll
+            for (int u = 0; u < kBatch; ++u) x[u] = k0 + u < nit ? src[(size_t)(k0 + u) * stride] : 0.f;
+#pragma unroll
+            for (int u = 0; u < kBatch; ++u) v += x[u];
+        }
         p.grad_value[((size_t)(n * p.S + st + h * W + w) * p.M + m) * D + ch] = v;
     }
 }
@@ -1445,7 +1467,7 @@ hipError_t launch_backward_value_binned(const Params& p0, msda_dtype_t dtype, hi
             else
                 hipLaunchKernelGGL((fold_runs_kernel<float, true>), dim3(grid), dim3(256), 0, stream, p);
             if ((e = hipGetLastError()) != hipSuccess) return e;
-            hipLaunchKernelGGL(split_reduce_kernel, dim3((unsigned)((p.n_tiles + 3) / 4)), dim3(256), 0, stream, p);
+            hipLaunchKernelGGL(split_reduce_kernel, dim3((unsigned)p.n_tiles), dim3(256), 0, stream, p);
         } else if (dtype == MSDA_F16) {
             hipLaunchKernelGGL((fold_runs_kernel<_Float16, false>), dim3(grid), dim3(256), 0, stream, p);
         } else {
