@@ -81,6 +81,14 @@ def test_full_size_bitwise_reproducible(name):
     assert np.array_equal(first["grad_value"].view(np.uint32), gv.cpu().numpy().view(np.uint32))
 
 
+@pytest.mark.parametrize("name", ["swin5_f16", "bev_sca", "detr_decoder"])
+def test_full_size_parity(name):
+    w = workloads.BY_NAME[name]
+    say(f"deterministic full-size parity {name}")
+    inp = workloads.generate(w)
+    check_parity(inp, gpu=run_det(inp))
+
+
 def test_empty_and_hot_key():
     import torch
 
