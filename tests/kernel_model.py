@@ -1,0 +1,238 @@
+"""Bounds-checked CPU model of the atomic backward's addressing (test infrastructure).
+
+The atomic grad_value variant of the backward kernel (grad_value accumulated with fp32 buffer
+atomics, Sec. 4.2's scatter-add done directly) is replayed here on the CPU exactly as the host
+code launches it and as each lane forms its addresses:
+
+  * the host's batch split (largest batch count per launch that keeps element offsets below
+    2^29) and the launch geometry (channels per lane, lanes per query, queries per wave, grid
+    padded to a multiple of 8);
+  * the workgroup -> (batch, head, query chunk) renumbering that keeps a slab on one XCD;
+  * the per-sample description: fp32 image coordinates, the open range test, floor, the int32
+    element offset of each corner row, and the out-of-range sentinel (2^29 elements) for corners
+    off the map, samples off the map and queries past Lq;
+  * every value-row load, grad_out read and grad_value atomic of every lane, with the buffer
+    resource's range rule (an access whose byte range ends past the resource's size returns 0 /
+    is dropped).
+
+Each access is checked: in-range accesses address a whole row of the right (batch, pixel, head)
+inside the launch's buffers, and every dropped access is one the definition says contributes
+nothing. The atomics that land are then summed in fp64 and compared with the oracle. The model
+imports neither the GPU library nor the oracle; the tests do the comparison.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass
+
+import numpy as np
+
+MAX_LAUNCH_ELEMS = 1 << 29  # per-launch element limit; also the off-map sentinel offset
+MAX_INDEX = (1 << 31) - 1
+WAVES_PER_BLOCK = 4
+U32 = 1 << 32
+
+
+def pick_vec(D: int, es: int) -> int:
+    """Channels per lane: the widest row piece (<= 16 bytes) that divides D."""
+    v = 16 // es
+    while v > 1:
+        if D % v == 0:
+            return v
+        v >>= 1
+    return 1
+
+
+def pick_lpp(D: int, vec: int) -> int:
+    """Lanes per query: enough VEC-wide pieces to cover D, rounded up to a power of two (<= 64)."""
+    need = (D + vec - 1) // vec
+    lpp = 1
+    while lpp < need and lpp < 64:
+        lpp <<= 1
+    return lpp
+
+
+def batch_per_launch(S, M, D, Lq, L, P) -> int:
+    nb = (MAX_LAUNCH_ELEMS - 1) // (S * M * D)
+    per_q = Lq * M * max(L * P * 2, D)
+    if per_q > 0 and MAX_INDEX // per_q < nb:
+        nb = MAX_INDEX // per_q
+    return max(nb, 1)
+
+
+def fmaf32(x: np.ndarray, s: int, c: float) -> np.ndarray:
+    """fp32 fma(x, s, c) with one rounding: x (fp32) * s (an integer below 2^24) is exact in the
+    64-bit significand of long double, and so is the sum with c = -0.5 for every |x*s| >= 2^-30;
+    below that both sides round to -0.5f."""
+    r = x.astype(np.longdouble) * np.longdouble(s) + np.longdouble(c)
+    return r.astype(np.float32)
+
+
+@dataclass
+class Launch:
+    n0: int
+    cnt: int
+    vec: int
+    lpp: int
+    ppw: int
+    q_per_block: int
+    chunks: int
+    num_blocks: int
+    grid: int
+
+
+class AddressError(AssertionError):
+    pass
+
+
+def launches(N, S, M, D, Lq, L, P, es):
+    nb = batch_per_launch(S, M, D, Lq, L, P)
+    vec = pick_vec(D, es)
+    lpp = pick_lpp(D, vec)
+    ppw = 64 // lpp
+    qpb = WAVES_PER_BLOCK * ppw
+    out = []
+    for n0 in range(0, N, nb):
+        cnt = min(nb, N - n0)
+        chunks = (Lq + qpb - 1) // qpb
+        num_blocks = cnt * M * chunks
+        grid = (num_blocks + 7) // 8 * 8
+        out.append(Launch(n0, cnt, vec, lpp, ppw, qpb, chunks, num_blocks, grid))
+    return out
+
+
+def _check(cond, msg):
+    if not bool(np.all(cond)):
+        raise AddressError(msg)
+
+
+def wave_queries(ln: Launch, M: int):
+    """(n, m, q) of every query slot of every wave of the launch, in the kernel's mapping
+    (workgroup b runs w = (b % 8) * (G / 8) + b / 8; slab-major work items)."""
+    b = np.arange(ln.grid, dtype=np.int64)
+    w = (b & 7) * (ln.grid >> 3) + (b >> 3)
+    _check(np.unique(w).size == ln.grid, "workgroup renumbering is not a permutation")
+    w = w[w < ln.num_blocks]
+    slab, chunk = w // ln.chunks, w % ln.chunks
+    n, m = slab // M, slab % M
+    wave = np.arange(WAVES_PER_BLOCK, dtype=np.int64)
+    ps = np.arange(ln.ppw, dtype=np.int64)
+    q = (chunk[:, None, None] * ln.q_per_block + wave[None, :, None] * ln.ppw + ps[None, None, :])
+    shp = q.shape
+    return (np.broadcast_to(n[:, None, None], shp).ravel(), np.broadcast_to(m[:, None, None], shp).ravel(),
+            q.ravel())
+
+
+def lane_channel_maps(D: int, vec: int, lpp: int):
+    """Channels read by value-row loads (lane sub, pass c0: [c0 + sub*vec, +vec)) and channels
+    added by the atomics (lane sub, pass c0, element i: c0 + sub + lpp*i), each checked to cover
+    [0, D) exactly once."""
+    loads, atom = [], []
+    for c0 in range(0, D, lpp * vec):
+        for sub in range(lpp):
+            chan = c0 + sub * vec
+            if chan < D:
+                loads.append((chan, vec))
+            for i in range(vec):
+                ct = c0 + sub + lpp * i
+                if ct < D:
+                    atom.append(ct)
+    cov = np.zeros(D, dtype=np.int64)
+    for chan, v in loads:
+        cov[chan:chan + v] += 1
+    _check(np.all(cov == 1), f"value-row loads do not cover the {D} channels once")
+    _check(sorted(atom) == list(range(D)), f"atomic lanes do not cover the {D} channels once")
+    return loads, atom
+
+
+def model_atomic_backward(value, shapes, starts, loc, attn, grad_out, plant_col_step=0):
+    """Replay the atomic backward's addressing on the CPU; returns grad_value (fp64) summed from
+    the atomics that land, and a dict of access counts. Raises AddressError on the first access
+    that breaks an invariant. plant_col_step adds a planted error to the column step of the
+    corner offsets (for the test that the model notices one)."""
+    import scipy.sparse as sp
+
+    N, S, M, D = value.shape
+    _, Lq, _, L, P, _ = loc.shape
+    K = L * P
+    es = value.dtype.itemsize
+    H = [int(h) for h, _ in shapes]
+    W = [int(w) for _, w in shapes]
+    st = [int(s) for s in starts]
+    gv = np.zeros((N * S * M, D), dtype=np.float64)
+    g = np.asarray(grad_out, dtype=np.float64).reshape(N * Lq * M, D)
+    stats = {"launches": 0, "sample_slots": 0, "tail_slots": 0, "corner_atomics_landed": 0,
+             "corner_atomics_dropped": 0}
+    lns = launches(N, S, M, D, Lq, L, P, es)
+    for ln in lns:
+        stats["launches"] += 1
+        loads, atom = lane_channel_maps(D, ln.vec, ln.lpp)
+        elems = ln.cnt * S * M * D
+        value_bytes, gv_bytes = elems * es, elems * 4
+        _check(elems < MAX_LAUNCH_ELEMS, "launch exceeds the element limit")
+        _check(ln.cnt * Lq * M * K * 2 <= MAX_INDEX and ln.cnt * Lq * M * D <= MAX_INDEX,
+               "per-launch sample index range exceeds int32")
+        n, m, q = wave_queries(ln, M)
+        # every real (n, m, q) of the launch is served exactly once; the rest are tail slots
+        real = q < Lq
+        key = (n[real] * M + m[real]) * Lq + q[real]
+        _check(np.unique(key).size == key.size == ln.cnt * M * Lq, "queries not covered exactly once")
+        stats["sample_slots"] += int(real.sum()) * K
+        stats["tail_slots"] += int((~real).sum()) * K
+        # grad_out row read by each query slot (tail slots read query 0's row)
+        gout_row = ((n * Lq + np.where(real, q, 0)) * M + m) * D
+        _check((gout_row >= 0) & (gout_row + D <= ln.cnt * Lq * M * D), "grad_out row out of range")
+        for k in range(K):
+            l = k // P
+            qq = np.where(real, q, 0)
+            smp = ((n * Lq + qq) * M + m) * K + k
+            _check(smp[real] < ln.cnt * Lq * M * K, "sample index out of range")
+            xy = loc[ln.n0:ln.n0 + ln.cnt].reshape(-1, 2)[smp]
+            a = attn[ln.n0:ln.n0 + ln.cnt].reshape(-1)[smp].astype(np.float32)
+            x = np.where(real, xy[:, 0], np.float32(-2.0)).astype(np.float32)
+            y = np.where(real, xy[:, 1], np.float32(-2.0)).astype(np.float32)
+            a = np.where(real, a, np.float32(0.0))
+            w_im = fmaf32(x, W[l], -0.5)
+            h_im = fmaf32(y, H[l], -0.5)
+            ok = (h_im > -1) & (w_im > -1) & (h_im < H[l]) & (w_im < W[l])
+            h0f, w0f = np.floor(h_im), np.floor(w_im)
+            h0 = np.where(ok, h0f, 0).astype(np.int64)
+            w0 = np.where(ok, w0f, 0).astype(np.int64)
+            lh = np.where(ok, h_im - h0f, 0).astype(np.float32)
+            lw = np.where(ok, w_im - w0f, 0).astype(np.float32)
+            hh, hw = np.float32(1) - lh, np.float32(1) - lw
+            a = np.where(ok, a, np.float32(0))
+            base = ((n * S + st[l] + h0 * W[l] + w0) * M + m) * D
+            _check(np.abs(base[ok]) <= MAX_INDEX, "corner base offset overflows int32")
+            top, bot, lef, rig = h0 >= 0, h0 + 1 < H[l], w0 >= 0, w0 + 1 < W[l]
+            corners = [(top & lef, base, a * (hh * hw)),
+                       (top & rig, base + M * D + plant_col_step, a * (hh * lw)),
+                       (bot & lef, base + W[l] * M * D, a * (lh * hw)),
+                       (bot & rig, base + (W[l] + 1) * M * D + plant_col_step, a * (lh * lw))]
+            for dh_dw, (cv, off_if, wgt) in zip(((0, 0), (0, 1), (1, 0), (1, 1)), corners):
+                valid = ok & cv
+                off = np.where(valid, off_if, MAX_LAUNCH_ELEMS).astype(np.int64)
+                # value-row loads: [(off << shift) + chan*es, + vec*es) against value_bytes
+                for chan, v in loads:
+                    lo_b = (off * es + chan * es) % U32
+                    _check(off * es + chan * es < U32, "value load offset wraps 32 bits")
+                    inr = lo_b + v * es <= value_bytes
+                    _check(inr == valid, "a value-row load lands iff its corner is on the map")
+                # the atomics: byte (off << 2) + ct*4 against gv_bytes
+                for ct in (atom[0], atom[-1]):
+                    byte = off * 4 + ct * 4
+                    _check(byte < U32, "atomic offset wraps 32 bits")
+                    _check((byte + 4 <= gv_bytes) == valid, "an atomic lands iff its corner is on the map")
+                # a landed corner is the row of pixel (h0+dh, w0+dw) of this (batch, head)
+                hc, wc = h0 + dh_dw[0], w0 + dh_dw[1]
+                want = ((n * S + st[l] + hc * W[l] + wc) * M + m) * D
+                _check(off[valid] == want[valid], "landed corner is not the sampled pixel's row")
+                _check(off[valid] % D == 0, "corner offset is not a row start")
+                stats["corner_atomics_landed"] += int(valid.sum()) * D
+                stats["corner_atomics_dropped"] += int((~valid).sum()) * D
+                # accumulate: grad_value[row] += w * g[query row]
+                rows = (off[valid] // D) + ln.n0 * S * M
+                cols = gout_row[valid] // D + ln.n0 * Lq * M
+                if rows.size:
+                    A = sp.coo_matrix((wgt[valid].astype(np.float64), (rows, cols)), shape=(N * S * M, N * Lq * M))
+                    gv += A.tocsr() @ g
+    return gv.reshape(N, S, M, D), stats
