@@ -10,7 +10,13 @@ import pytest
 import oracle
 from paper_2505_14022_amd import msda, workloads
 
-# Tolerances: normwise per tensor, max_i |gpu_i - ref_i| / max_i |ref_i|.
+# Tolerances: normwise per tensor, max_i |gpu_i - ref_i| / max_i |ref_i|, and a bound on the 99.9th
+# percentile of the element-wise relative error (elementwise_p999): the same value for every output
+# except fp32 out, whose bound is ten times its normwise one. An fp32 sum of 4*L*P weighted corner
+# values that cancels down to a few thousandths of the largest output keeps the absolute rounding
+# error of its terms: measured 1.0e-5 .. 3.2e-5 at the 0.999 quantile for 16 .. 576 terms, every
+# gradient below a tenth of its bound.
+TOL_P999_OUT_F32 = 1e-4
 TOL_OUT_F32 = 1e-5
 TOL_OUT_F16 = 1e-3
 TOL_GRAD_VALUE = 1e-4
@@ -41,6 +47,41 @@ def normwise(gpu, ref) -> float:
     if scale == 0.0:
         return err
     return err / scale
+
+
+def elementwise_p999(gpu, ref) -> float:
+    """99.9th percentile over elements of |gpu_i - ref_i| / max(|ref_i|, 1e-3 * max_j |ref_j|): the
+    element-wise relative error, with a floor that keeps elements whose exact value cancels to
+    nearly zero from dividing by zero (the normwise error covers those)."""
+    gpu = np.asarray(gpu, dtype=np.float64).ravel()
+    ref = np.asarray(ref, dtype=np.float64).ravel()
+    if ref.size == 0:
+        return 0.0
+    scale = float(np.max(np.abs(ref)))
+    floor = 1e-3 * scale if scale > 0.0 else 1.0
+    rel = np.abs(gpu - ref) / np.maximum(np.abs(ref), floor)
+    return float(np.quantile(rel, 0.999))
+
+
+# Full-size cases record one line each here (entry point, workload, normwise and p99.9 error per
+# output); tests/conftest.py prints them at the end of the run, entry points in this order.
+SUMMARY = {}
+ENTRY_ORDER = ("msda_backward", "fused", "deterministic", "atomic", "owner")
+_SHORT = {"out": "out", "grad_value": "gv", "grad_loc": "gl", "grad_attn": "ga", "grad_offsets": "goff",
+          "grad_logits": "glog", "grad_ref": "gref"}
+
+
+def record(entry: str, name: str, errs: dict, p999: dict):
+    if name in workloads.BY_NAME:
+        SUMMARY[(entry, name)] = f"{entry[:13]:<13} {name:<12} " + " ".join(
+            f"{_SHORT.get(k, k)} {errs[k]:.0e}/{p999[k]:.0e}" for k in errs)
+
+
+def summary_lines():
+    rank = {e: i for i, e in enumerate(ENTRY_ORDER)}
+    wl = {w.name: i for i, w in enumerate(workloads.WORKLOADS)}
+    keys = sorted(SUMMARY, key=lambda k: (rank.get(k[0], 99), wl.get(k[1], 99)))
+    return [SUMMARY[k] for k in keys]
 
 
 @dataclass
@@ -84,8 +125,10 @@ def run_oracle(inp: workloads.Inputs, backward: bool = True):
     return res
 
 
-def check_parity(inp: workloads.Inputs, backward: bool = True, gpu=None, ref=None, workspace="auto"):
-    """Element-by-element comparison of every output; returns the error table."""
+def check_parity(inp: workloads.Inputs, backward: bool = True, gpu=None, ref=None, workspace="auto",
+                 entry: str = ""):
+    """Element-by-element comparison of every output; returns the error table. `entry` names the
+    backward entry point for the run summary (default: the plain one with `workspace`)."""
     fp16 = inp.value.dtype == np.float16
     gpu = gpu or run_gpu(inp, backward, workspace)
     ref = ref or run_oracle(inp, backward)
@@ -103,7 +146,9 @@ def check_parity(inp: workloads.Inputs, backward: bool = True, gpu=None, ref=Non
         for k, t in (("grad_value", TOL_GRAD_VALUE), ("grad_loc", TOL_GRAD_LOC), ("grad_attn", TOL_GRAD_ATTN)):
             errs[k] = normwise(gpu[k], ref[k])
             tols[k] = t
-    say(f"  {inp.w.name}: " + ", ".join(f"{k} {errs[k]:.2e} (tol {tols[k]:.0e})" for k in errs))
+    p999 = {k: elementwise_p999(gpu[k], ref[k]) for k in errs}
+    say(f"  {inp.w.name}: " + ", ".join(f"{k} {errs[k]:.2e} p99.9 {p999[k]:.2e} (tol {tols[k]:.0e})" for k in errs))
+    record(entry or {None: "atomic", "owner": "owner"}.get(workspace, "msda_backward"), inp.w.name, errs, p999)
     for k in errs:
         assert gpu[k].shape == tuple(ref[k].shape), f"{k}: shape {gpu[k].shape} vs {ref[k].shape}"
         assert np.all(np.isfinite(gpu[k])), f"{inp.w.name}: non-finite values in {k}"
@@ -115,6 +160,8 @@ def check_parity(inp: workloads.Inputs, backward: bool = True, gpu=None, ref=Non
             raise AssertionError(f"{inp.w.name}: {k} normwise error {errs[k]:.3e} > {tols[k]:.0e}; worst at {i}: "
                                  f"gpu {float(gpu[k][i]):.6g} ref {float(ref[k][i]):.6g}; {nbad} of {d.size} "
                                  f"elements off; <gpu,ref>/<ref,ref> = {ratio:.4f}")
+        tp = TOL_P999_OUT_F32 if (k == "out" and not fp16) else tols[k]
+        assert p999[k] <= tp, f"{inp.w.name}: {k} 99.9th-percentile element-wise error {p999[k]:.3e} > {tp:.0e}"
     return errs
 
 
@@ -163,11 +210,16 @@ def check_parity_fused(inp: workloads.FusedInputs, workspace="auto", want_grad_r
         assert gpu[k].shape == tuple(ref[k].shape), f"{k}: shape {gpu[k].shape} vs {ref[k].shape}"
         assert np.all(np.isfinite(gpu[k])), f"{inp.w.name}: non-finite values in {k}"
         errs[k] = normwise(gpu[k], ref[k])
-    say(f"  {inp.w.name} (fused): " + ", ".join(f"{k} {errs[k]:.2e} (tol {tols[k]:.0e})" for k in errs))
+    p999 = {k: elementwise_p999(gpu[k], ref[k]) for k in errs}
+    say(f"  {inp.w.name} (fused): " + ", ".join(f"{k} {errs[k]:.2e} p99.9 {p999[k]:.2e} (tol {tols[k]:.0e})"
+                                               for k in errs))
+    record("fused", inp.w.name, errs, p999)
     for k, t in tols.items():
         if errs[k] > t:
             d = np.abs(gpu[k].astype(np.float64) - ref[k])
             i = np.unravel_index(int(np.argmax(d)), d.shape)
             raise AssertionError(f"{inp.w.name}: {k} normwise error {errs[k]:.3e} > {t:.0e}; worst at {i}: "
                                  f"gpu {float(gpu[k][i]):.6g} ref {float(ref[k][i]):.6g}")
+        tp = TOL_P999_OUT_F32 if (k == "out" and not fp16) else t
+        assert p999[k] <= tp, f"{inp.w.name}: {k} 99.9th-percentile element-wise error {p999[k]:.3e} > {tp:.0e}"
     return errs

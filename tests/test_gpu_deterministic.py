@@ -42,7 +42,7 @@ def test_small_parity(case):
     N, M, D, shapes, P, Lq, dt = case
     inp = workloads.random_case(N, M, D, shapes, P, Lq, dt, seed=3000 + D + Lq)
     say(f"deterministic small case {inp.w.name}")
-    check_parity(inp, gpu=run_det(inp))
+    check_parity(inp, gpu=run_det(inp), entry="deterministic")
 
 
 @pytest.mark.parametrize("seed", range(2))
@@ -53,7 +53,7 @@ def test_split_tiles_parity_and_bits(seed):
     say(f"deterministic split tiles seed {seed}")
     d = to_device(inp)
     a = run_det(inp, d)
-    check_parity(inp, gpu=a)
+    check_parity(inp, gpu=a, entry="deterministic")
     b = run_det(inp, d)
     assert np.array_equal(a["grad_value"].view(np.uint32), b["grad_value"].view(np.uint32))
 
@@ -67,7 +67,7 @@ def test_full_size_bitwise_reproducible(name):
     inp = workloads.generate(w)
     d = to_device(inp)
     first = run_det(inp, d)
-    check_parity(inp, gpu=first)
+    check_parity(inp, gpu=first, entry="deterministic")
     # other work in between: the default backward (atomics on split tiles, records in arrival order)
     # and a side stream, then the deterministic backward again, twice
     msda.backward(d.value, inp.shapes, inp.starts, d.loc, d.attn, d.grad_out)
@@ -81,12 +81,12 @@ def test_full_size_bitwise_reproducible(name):
     assert np.array_equal(first["grad_value"].view(np.uint32), gv.cpu().numpy().view(np.uint32))
 
 
-@pytest.mark.parametrize("name", ["swin5_f16", "bev_sca", "detr_decoder"])
+@pytest.mark.parametrize("name", ["swin5_f16", "bev_sca", "detr_decoder", "tiny"])
 def test_full_size_parity(name):
     w = workloads.BY_NAME[name]
     say(f"deterministic full-size parity {name}")
     inp = workloads.generate(w)
-    check_parity(inp, gpu=run_det(inp))
+    check_parity(inp, gpu=run_det(inp), entry="deterministic")
 
 
 def test_empty_and_hot_key():
@@ -103,6 +103,6 @@ def test_empty_and_hot_key():
 
     inp = _hot_cell_case(352, 148, seed=77)
     say("deterministic hot key")
-    check_parity(inp, gpu=run_det(inp))
+    check_parity(inp, gpu=run_det(inp), entry="deterministic")
     ref = run_oracle(inp)
     assert ref["grad_value"].shape == inp.value.shape
