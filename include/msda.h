@@ -30,15 +30,21 @@
  *
  * Ownership and execution. All tensor pointers are DEVICE pointers owned by the caller, except the
  * two level tables, which are HOST pointers read during the call. The library allocates no device
- * memory (the backward's scratch is a caller-provided workspace), never synchronizes and never
- * prints. Work is enqueued on `stream` (a hipStream_t; NULL means the default stream) and the call
- * returns before it completes. The owner-computes backward runs its grad_value kernels on a second
- * stream, forked from `stream` at the start of the call and joined back into it before the call's
- * last work item, so everything enqueued on `stream` afterwards is ordered after all of the call's
- * work (also under stream capture). That stream and its two events are the only state the library
- * keeps: one set per (host thread, device), created by the first such call and kept for the life of
- * the thread; if they cannot be created the call runs on `stream` alone. Outputs are overwritten
- * entirely and must not alias inputs or the workspace. Inputs are not modified.
+ * memory (the owner-computes backward's scratch is a caller-provided workspace), never
+ * synchronizes and never prints. Work is enqueued on `stream` (a hipStream_t of any device; NULL
+ * means the current device's null stream) and the call returns before it completes. Outputs are
+ * overwritten entirely and must not alias inputs or the workspace. Inputs are not modified.
+ *
+ * State kept between calls (a deviation from a stateless library, for speed): the owner-computes
+ * backward (msda_backward and msda_backward_deterministic with a workspace, msda_backward_fused
+ * with the owner-computes part of its workspace) runs its grad_value kernels on a second stream,
+ * forked from `stream` at the start of the call and joined back into it before the call's last
+ * work item, so everything enqueued on `stream` afterwards is ordered after all of the call's work
+ * (also under stream capture). That stream and its two events belong to the library: one set per
+ * device (the device of `stream`), created by the first such call on that device, shared by all
+ * host threads (a lock covers each call's fork and join), and destroyed by msda_release(). If they
+ * cannot be created the call runs on `stream` alone. No other entry point keeps any state.
+ *
  * Arithmetic is fp32 (fp16 inputs are converted exactly; fp16 out is rounded to nearest-even
  * once). The order in which contributions to one grad_value element are summed depends on
  * scheduling, so its low bits may differ between runs; out, grad_loc and grad_attn are
@@ -102,12 +108,14 @@ msda_status_t msda_forward(const void* value, const int64_t* spatial_shapes,
  *
  * workspace: DEVICE scratch of at least the size msda_backward_workspace_size(...,
  * MSDA_WORKSPACE_OWNER, ...) reports, 256-byte aligned, owned by the caller and not used by
- * anything else until the enqueued work completes. With a workspace, grad_value is computed
- * owner-by-owner: samples are sorted by the pixel tile they touch and each grad_value row is
- * written once by the wave that owns its tile (rows of tiles seen by more than one chunk of 512
- * samples are added with atomics). With workspace == NULL, or when the owner-computes path does
- * not apply, grad_value is zeroed and accumulated with fp32 atomics. A non-null workspace smaller
- * than required is an error.
+ * anything else until the enqueued work completes. grad_value is then computed owner-by-owner:
+ * samples are sorted by the pixel tile they touch and each grad_value row is written once by the
+ * wave that owns its tile (rows of tiles seen by more than one chunk of 512 samples are added with
+ * atomics). workspace may be NULL only where msda_backward_workspace_size(...,
+ * MSDA_WORKSPACE_PREFERRED, ...) reports 0 bytes (small or sparse problems, and problems the
+ * owner-computes path does not apply to): there grad_value is zeroed and accumulated with fp32
+ * atomics, as msda_backward_atomic does. Anywhere else a NULL workspace, or one smaller than
+ * required, is MSDA_ERROR_INVALID_VALUE: the library never switches algorithms silently.
  *
  * value and grad_out 16-byte aligned; grad_value 16-byte; grad_loc 8-byte; grad_attn 4-byte.
  * N*Lq == 0 still zeroes grad_value.
@@ -118,6 +126,22 @@ msda_status_t msda_backward(const void* value, const int64_t* spatial_shapes,
                             float* grad_loc, float* grad_attn, void* workspace, size_t workspace_bytes,
                             int64_t N, int64_t S, int64_t M, int64_t D, int64_t Lq, int64_t L,
                             int64_t P, int dtype, void* stream);
+
+/*
+ * Backward pass with grad_value accumulated by fp32 atomics (Sec. 4.2's scatter-add done
+ * directly): the same arguments, layouts and results as msda_backward, without a workspace.
+ * grad_value is zeroed, then every valid corner of every sample adds a * w_corner * grad_out to
+ * its row with fp32 device atomics; the summation order, and so the low bits of grad_value, vary
+ * between runs. Nothing is kept between calls and only `stream` is used. It is the fast choice
+ * for sparse problems (fewer samples than value rows); on dense ones msda_backward is an order of
+ * magnitude faster. value and grad_out 16-byte aligned; grad_value 16-byte; grad_loc 8-byte;
+ * grad_attn 4-byte. N*Lq == 0 still zeroes grad_value.
+ */
+msda_status_t msda_backward_atomic(const void* value, const int64_t* spatial_shapes,
+                                   const int64_t* level_start_index, const float* sampling_loc,
+                                   const float* attn_weight, const void* grad_out, float* grad_value,
+                                   float* grad_loc, float* grad_attn, int64_t N, int64_t S, int64_t M,
+                                   int64_t D, int64_t Lq, int64_t L, int64_t P, int dtype, void* stream);
 
 /*
  * Backward pass with a bitwise reproducible grad_value: the same as msda_backward (same arguments,
@@ -235,6 +259,14 @@ const char* msda_last_error(void);
 
 /* Library version as major*10000 + minor*100 + patch. */
 int msda_version(void);
+
+/*
+ * Destroys the side streams and events the owner-computes backward created (one set per device;
+ * see "State kept between calls" above), after waiting for the work enqueued on them. Call it only
+ * when no libmsda work is being enqueued by another thread; a later backward call creates what it
+ * needs again. MSDA_ERROR_LAUNCH_FAILED if the runtime reports an error while releasing.
+ */
+msda_status_t msda_release(void);
 
 #ifdef __cplusplus
 }

@@ -3,6 +3,8 @@
 #include <stdint.h>
 #include <stdio.h>
 
+#include <mutex>
+
 #include <hip/hip_runtime.h>
 
 #include "msda.h"
@@ -131,8 +133,10 @@ size_t fused_staging_bytes(int64_t N, int64_t S, int64_t M, int64_t D, int64_t L
 // A second stream for the backward: the grad_value pipeline (binning and fold) and the
 // grad_loc / grad_attn kernel read the same inputs and write disjoint outputs, so they run side by
 // side, forked from and joined back into the caller's stream with two events. One stream and two
-// events per (host thread, device), created on first use and kept for the life of the thread; if
-// they cannot be created the backward runs on the caller's stream alone.
+// events per device, created by the first backward call on that device (the device of the caller's
+// stream) and kept until msda_release(). If they cannot be created the backward runs on the
+// caller's stream alone. The mutex is held from the fork to the join of a call, so calls from
+// several host threads never interleave their event records.
 struct SideStream {
     hipStream_t s = nullptr;
     hipEvent_t fork = nullptr, join = nullptr;
@@ -141,14 +145,35 @@ struct SideStream {
 constexpr int kMaxDevices = 64;
 // The events order work between two streams of one device: a device-scope fence is enough.
 constexpr unsigned kSideEventFlags = hipEventDisableTiming | hipEventDisableSystemFence;
+std::mutex g_side_mutex;
+SideStream g_side[kMaxDevices];
 
-SideStream* side_stream() {
-    int dev = 0;
-    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
-    thread_local SideStream table[kMaxDevices];
-    SideStream& x = table[dev];
+// The device the caller's stream belongs to (the current device for the null stream), or -1.
+int stream_device(hipStream_t stream) {
+    int dev = -1;
+    if (stream) {
+        hipDevice_t d = -1;
+        if (hipStreamGetDevice(stream, &d) != hipSuccess) return -1;
+        dev = (int)d;
+    } else if (hipGetDevice(&dev) != hipSuccess) {
+        return -1;
+    }
+    return dev >= 0 && dev < kMaxDevices ? dev : -1;
+}
+
+// The side stream of `dev` (created on first use, with `dev` made current meanwhile), or null.
+// Called with g_side_mutex held.
+SideStream* side_stream(int dev) {
+    if (dev < 0) return nullptr;
+    SideStream& x = g_side[dev];
     if (!x.tried) {
         x.tried = true;
+        int cur = -1;
+        const bool switch_dev = hipGetDevice(&cur) == hipSuccess && cur != dev;
+        if (switch_dev && hipSetDevice(dev) != hipSuccess) {
+            (void)hipGetLastError();
+            return nullptr;
+        }
         if (hipStreamCreateWithFlags(&x.s, hipStreamNonBlocking) != hipSuccess) {
             x.s = nullptr;
         } else if (hipEventCreateWithFlags(&x.fork, kSideEventFlags) != hipSuccess ||
@@ -156,7 +181,9 @@ SideStream* side_stream() {
             if (x.fork) (void)hipEventDestroy(x.fork);
             (void)hipStreamDestroy(x.s);
             x.s = nullptr;
+            x.fork = nullptr;
         }
+        if (switch_dev) (void)hipSetDevice(cur);
         (void)hipGetLastError();  // a failed creation leaves nothing for the next call to report
     }
     return x.s ? &x : nullptr;
@@ -169,7 +196,7 @@ SideStream* side_stream() {
 msda_status_t backward_body(const void* value, const int64_t* shapes, const int64_t* starts, const void* grad_out,
                             float* grad_value, const Sampling& smp, const Prologue* pro, void* workspace, int64_t N,
                             int64_t S, int64_t M, int64_t D, int64_t Lq, int64_t L, int64_t P, int dtype,
-                            hipStream_t s, bool deterministic = false) {
+                            hipStream_t s, bool deterministic = false, bool one_stream = false) {
     if (!grad_value) return fail(MSDA_ERROR_INVALID_VALUE, "grad_value must be non-null");
     if (!aligned(grad_value, 16)) return fail(MSDA_ERROR_INVALID_VALUE, "misaligned grad_value: 16 bytes needed");
     if (Lq == 0) {
@@ -183,6 +210,15 @@ msda_status_t backward_body(const void* value, const int64_t* shapes, const int6
     const bool binned = workspace != nullptr;
     const int es = elem_size(dtype);
     const int64_t nb = batch_per_launch(S, M, D, Lq, L, P);
+    // the owner-computes grad_value runs beside grad_loc / grad_attn on the side stream of the
+    // caller's stream's device; the lock spans every fork and join this call enqueues
+    std::unique_lock<std::mutex> side_lock(g_side_mutex, std::defer_lock);
+    SideStream* side = nullptr;
+    if (binned && !one_stream) {
+        side_lock.lock();
+        side = side_stream(stream_device(s));
+        if (!side) side_lock.unlock();
+    }
     if (!binned) {
         hipError_t e = msda::launch_zero(grad_value, N * S * M * D, s);
         if (e != hipSuccess) return fail(MSDA_ERROR_LAUNCH_FAILED, "grad_value zeroing: %s", hipGetErrorString(e));
@@ -230,7 +266,6 @@ msda_status_t backward_body(const void* value, const int64_t* shapes, const int6
                 return fail(MSDA_ERROR_LAUNCH_FAILED, "workspace reset: %s", hipGetErrorString(e));
         }
         // grad_value (binned) on the side stream, forked after everything enqueued on `s` so far
-        SideStream* side = binned ? side_stream() : nullptr;
         if (side && ((e = hipEventRecord(side->fork, s)) != hipSuccess ||
                      (e = hipStreamWaitEvent(side->s, side->fork, 0)) != hipSuccess))
             return fail(MSDA_ERROR_LAUNCH_FAILED, "backward fork: %s", hipGetErrorString(e));
@@ -342,21 +377,53 @@ msda_status_t msda_backward(const void* value, const int64_t* spatial_shapes, co
                         "attn_weight and grad_attn 4");
     }
     bool binned = false;
-    if (workspace && Lq > 0) {
+    if (Lq > 0) {
         size_t need = 0;
         msda_backward_workspace_size(spatial_shapes, level_start_index, N, S, M, D, Lq, L, P, dtype,
                                      MSDA_WORKSPACE_OWNER, &need);
-        if (need > 0) {
+        if (need > 0 && workspace) {
             if (workspace_bytes < need)
                 return fail(MSDA_ERROR_INVALID_VALUE, "workspace of %zu bytes is smaller than the %zu needed",
                             workspace_bytes, need);
             if (!aligned(workspace, 256)) return fail(MSDA_ERROR_INVALID_VALUE, "workspace must be 256-byte aligned");
             binned = true;
+        } else if (need > 0) {
+            // no workspace: only where the library itself prefers fp32 atomics (small or sparse
+            // problems); elsewhere the caller chooses msda_backward_atomic explicitly
+            size_t preferred = 0;
+            msda_backward_workspace_size(spatial_shapes, level_start_index, N, S, M, D, Lq, L, P, dtype,
+                                         MSDA_WORKSPACE_PREFERRED, &preferred);
+            if (preferred > 0)
+                return fail(MSDA_ERROR_INVALID_VALUE,
+                            "msda_backward needs a workspace of %zu bytes for this problem (or call "
+                            "msda_backward_atomic)", preferred);
         }
     }
     Sampling smp = {sampling_loc, attn_weight, grad_loc, grad_attn};
     return backward_body(value, spatial_shapes, level_start_index, grad_out, grad_value, smp, nullptr,
                          binned ? workspace : nullptr, N, S, M, D, Lq, L, P, dtype, (hipStream_t)stream);
+}
+
+msda_status_t msda_backward_atomic(const void* value, const int64_t* spatial_shapes,
+                                   const int64_t* level_start_index, const float* sampling_loc,
+                                   const float* attn_weight, const void* grad_out, float* grad_value,
+                                   float* grad_loc, float* grad_attn, int64_t N, int64_t S, int64_t M, int64_t D,
+                                   int64_t Lq, int64_t L, int64_t P, int dtype, void* stream) {
+    msda_status_t st = check_problem(spatial_shapes, level_start_index, N, S, M, D, Lq, L, P, dtype);
+    if (st != MSDA_SUCCESS) return st;
+    if (N == 0) return ok();
+    if (Lq > 0) {
+        if (!sampling_loc || !attn_weight || !grad_loc || !grad_attn)
+            return fail(MSDA_ERROR_INVALID_VALUE,
+                        "value, sampling_loc, attn_weight, grad_out, grad_loc and grad_attn must be non-null");
+        if (!aligned(sampling_loc, 8) || !aligned(grad_loc, 8) || !aligned(attn_weight, 4) || !aligned(grad_attn, 4))
+            return fail(MSDA_ERROR_INVALID_VALUE,
+                        "misaligned pointer: value and grad_out need 16 bytes, sampling_loc and grad_loc 8, "
+                        "attn_weight and grad_attn 4");
+    }
+    Sampling smp = {sampling_loc, attn_weight, grad_loc, grad_attn};
+    return backward_body(value, spatial_shapes, level_start_index, grad_out, grad_value, smp, nullptr, nullptr, N,
+                         S, M, D, Lq, L, P, dtype, (hipStream_t)stream);
 }
 
 msda_status_t msda_backward_deterministic(const void* value, const int64_t* spatial_shapes,
@@ -491,6 +558,29 @@ const char* msda_status_string(msda_status_t status) {
 
 const char* msda_last_error(void) { return g_last_error; }
 
-int msda_version(void) { return 100; }
+msda_status_t msda_release(void) {
+    std::lock_guard<std::mutex> lock(g_side_mutex);
+    int cur = -1;
+    const bool have_cur = hipGetDevice(&cur) == hipSuccess;
+    hipError_t first = hipSuccess;
+    for (int dev = 0; dev < kMaxDevices; ++dev) {
+        SideStream& x = g_side[dev];
+        if (x.s) {
+            hipError_t e = hipSetDevice(dev);
+            if (e == hipSuccess) e = hipStreamSynchronize(x.s);
+            if (e == hipSuccess) e = hipEventDestroy(x.fork);
+            if (e == hipSuccess) e = hipEventDestroy(x.join);
+            if (e == hipSuccess) e = hipStreamDestroy(x.s);
+            if (e != hipSuccess && first == hipSuccess) first = e;
+        }
+        x = SideStream();
+    }
+    if (have_cur) (void)hipSetDevice(cur);
+    (void)hipGetLastError();
+    if (first != hipSuccess) return fail(MSDA_ERROR_LAUNCH_FAILED, "releasing the side streams: %s", hipGetErrorString(first));
+    return ok();
+}
+
+int msda_version(void) { return 200; }
 
 }  // extern "C"

@@ -1356,11 +1356,18 @@ size_t align256(size_t x) { return (x + 255) / 256 * 256; }
 // Workgroups to launch for a queue-driven kernel: two per CU, as many as the fold's LDS lets be
 // resident. (Four or eight per CU, the extra ones exiting at once when they find the queues drained,
 // made the backward 0.5-1 % and 3-7 % slower.)
-int queue_grid() {
+int queue_grid(hipStream_t stream) {
     constexpr int kDevs = 64;
     static std::atomic<int> cache[kDevs];
+    // the device the work is enqueued on: the stream's (the current device for the null stream)
     int dev = 0;
-    if (hipGetDevice(&dev) != hipSuccess) return -1;
+    if (stream) {
+        hipDevice_t d = 0;
+        if (hipStreamGetDevice(stream, &d) != hipSuccess) return -1;
+        dev = (int)d;
+    } else if (hipGetDevice(&dev) != hipSuccess) {
+        return -1;
+    }
     if (dev >= 0 && dev < kDevs) {
         const int c = cache[dev].load(std::memory_order_relaxed);
         if (c > 0) return c;
@@ -1460,7 +1467,7 @@ hipError_t launch_backward_value_binned(const Params& p0, msda_dtype_t dtype, hi
     else hipLaunchKernelGGL(bin_scatter_kernel<false>, scatter_grid, dim3(256), hist_lds, stream, p);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     if (p.D % 4 == 0) {
-        const int grid = queue_grid();  // the waves take work items from the queue
+        const int grid = queue_grid(stream);  // the waves take work items from the queue
         if (grid <= 0) return hipErrorInvalidConfiguration;
         if (det) {
             if (dtype == MSDA_F16)

@@ -26,10 +26,10 @@ MSDA_WORKSPACE_PREFERRED = 0
 MSDA_WORKSPACE_OWNER = 1
 MSDA_WORKSPACE_DETERMINISTIC = 2
 
-EXPORTED = ["msda_check_args", "msda_forward", "msda_backward", "msda_backward_deterministic",
-            "msda_backward_workspace_size",
+EXPORTED = ["msda_check_args", "msda_forward", "msda_backward", "msda_backward_atomic",
+            "msda_backward_deterministic", "msda_backward_workspace_size",
             "msda_forward_fused", "msda_backward_fused_workspace_size", "msda_backward_fused",
-            "msda_status_string", "msda_last_error", "msda_version"]
+            "msda_status_string", "msda_last_error", "msda_version", "msda_release"]
 
 
 class MsdaError(RuntimeError):
@@ -56,6 +56,8 @@ def lib():
         L.msda_backward.argtypes = [vp, ip, ip, vp, vp, vp, vp, vp, vp, vp, ctypes.c_size_t] + [i64] * 7 + \
             [ctypes.c_int, vp]
         L.msda_backward.restype = ctypes.c_int
+        L.msda_backward_atomic.argtypes = [vp, ip, ip, vp, vp, vp, vp, vp, vp] + [i64] * 7 + [ctypes.c_int, vp]
+        L.msda_backward_atomic.restype = ctypes.c_int
         L.msda_backward_deterministic.argtypes = L.msda_backward.argtypes
         L.msda_backward_deterministic.restype = ctypes.c_int
         L.msda_backward_workspace_size.argtypes = [ip, ip] + [i64] * 7 + [ctypes.c_int, ctypes.c_int,
@@ -74,6 +76,8 @@ def lib():
         L.msda_last_error.restype = ctypes.c_char_p
         L.msda_version.argtypes = []
         L.msda_version.restype = ctypes.c_int
+        L.msda_release.argtypes = []
+        L.msda_release.restype = ctypes.c_int
         _lib = L
     return _lib
 
@@ -84,6 +88,11 @@ def status_string(status: int) -> str:
 
 def last_error() -> str:
     return lib().msda_last_error().decode()
+
+
+def release():
+    """msda_release: destroy the library's side streams and events (after their work is done)."""
+    _raise(lib().msda_release(), "msda_release")
 
 
 def _host_tables(spatial_shapes, level_start_index) -> Tuple[np.ndarray, np.ndarray]:
@@ -115,6 +124,20 @@ def _stream(stream) -> Optional[int]:
 
         return torch.cuda.current_stream().cuda_stream
     return int(getattr(stream, "cuda_stream", stream))
+
+
+def _on(stream):
+    """A context under which torch allocates memory for use on `stream` (torch's current stream when
+    it is None). Outputs and workspaces the binding allocates are used by the kernels enqueued on
+    `stream`: allocated under another stream, the caching allocator could hand their memory to a
+    later allocation on that stream as soon as the binding returns, while the kernels still run."""
+    import torch
+
+    if stream is None:
+        return torch.cuda.stream(torch.cuda.current_stream())
+    if isinstance(stream, torch.cuda.Stream):
+        return torch.cuda.stream(stream)
+    return torch.cuda.stream(torch.cuda.ExternalStream(_stream(stream)))
 
 
 def _dtype_code(t) -> int:
@@ -166,7 +189,8 @@ def forward(value, spatial_shapes, level_start_index, sampling_loc, attn_weight,
 
     N, S, M, D, Lq, L, P = _dims(value, sampling_loc)
     if out is None:
-        out = torch.empty((N, Lq, M * D), dtype=value.dtype, device=value.device)
+        with _on(stream):
+            out = torch.empty((N, Lq, M * D), dtype=value.dtype, device=value.device)
     sh, st = _host_tables(spatial_shapes, level_start_index)
     r = lib().msda_forward(_dptr(value), _iptr(sh), _iptr(st), _dptr(sampling_loc), _dptr(attn_weight),
                            _dptr(out), N, S, M, D, Lq, L, P, _dtype_code(value), _stream(stream))
@@ -179,26 +203,35 @@ def backward(value, spatial_shapes, level_start_index, sampling_loc, attn_weight
     """(grad_value fp32, grad_loc, grad_attn) from msda_backward.
 
     workspace: "auto" allocates the workspace the library prefers for this problem (none where
-    atomics are faster), "owner" the owner-computes workspace wherever that path applies, None
-    passes no workspace (grad_value by atomics); or a caller-owned uint8 device tensor.
+    atomics are faster), "owner" the owner-computes workspace wherever that path applies, or a
+    caller-owned uint8 device tensor; None calls msda_backward_atomic (grad_value by fp32 atomics,
+    no workspace).
     """
     import torch
 
     N, S, M, D, Lq, L, P = _dims(value, sampling_loc)
     dev = value.device
-    if grad_value is None:
-        grad_value = torch.empty((N, S, M, D), dtype=torch.float32, device=dev)
-    if grad_loc is None:
-        grad_loc = torch.empty(tuple(sampling_loc.shape), dtype=torch.float32, device=dev)
-    if grad_attn is None:
-        grad_attn = torch.empty(tuple(attn_weight.shape), dtype=torch.float32, device=dev)
     sh, st = _host_tables(spatial_shapes, level_start_index)
-    if isinstance(workspace, str):
-        if workspace not in ("auto", "owner"):
-            raise ValueError(f"workspace must be 'auto', 'owner', None or a tensor, not {workspace!r}")
-        mode = MSDA_WORKSPACE_PREFERRED if workspace == "auto" else MSDA_WORKSPACE_OWNER
-        nbytes = workspace_size(sh.reshape(-1, 2), st, N, S, M, D, Lq, L, P, _dtype_code(value), mode)
-        workspace = torch.empty(max(nbytes, 1), dtype=torch.uint8, device=dev) if nbytes else None
+    with _on(stream):
+        if grad_value is None:
+            grad_value = torch.empty((N, S, M, D), dtype=torch.float32, device=dev)
+        if grad_loc is None:
+            grad_loc = torch.empty(tuple(sampling_loc.shape), dtype=torch.float32, device=dev)
+        if grad_attn is None:
+            grad_attn = torch.empty(tuple(attn_weight.shape), dtype=torch.float32, device=dev)
+        atomic = workspace is None
+        if isinstance(workspace, str):
+            if workspace not in ("auto", "owner"):
+                raise ValueError(f"workspace must be 'auto', 'owner', None or a tensor, not {workspace!r}")
+            mode = MSDA_WORKSPACE_PREFERRED if workspace == "auto" else MSDA_WORKSPACE_OWNER
+            nbytes = workspace_size(sh.reshape(-1, 2), st, N, S, M, D, Lq, L, P, _dtype_code(value), mode)
+            workspace = torch.empty(max(nbytes, 1), dtype=torch.uint8, device=dev) if nbytes else None
+    if atomic:
+        r = lib().msda_backward_atomic(_dptr(value), _iptr(sh), _iptr(st), _dptr(sampling_loc), _dptr(attn_weight),
+                                       _dptr(grad_out), _dptr(grad_value), _dptr(grad_loc), _dptr(grad_attn),
+                                       N, S, M, D, Lq, L, P, _dtype_code(value), _stream(stream))
+        _raise(r, "msda_backward_atomic")
+        return grad_value, grad_loc, grad_attn
     ws_ptr = _dptr(workspace) if workspace is not None else None
     ws_bytes = workspace.numel() * workspace.element_size() if workspace is not None else 0
     r = lib().msda_backward(_dptr(value), _iptr(sh), _iptr(st), _dptr(sampling_loc), _dptr(attn_weight),
@@ -217,17 +250,18 @@ def backward_deterministic(value, spatial_shapes, level_start_index, sampling_lo
 
     N, S, M, D, Lq, L, P = _dims(value, sampling_loc)
     dev = value.device
-    if grad_value is None:
-        grad_value = torch.empty((N, S, M, D), dtype=torch.float32, device=dev)
-    if grad_loc is None:
-        grad_loc = torch.empty(tuple(sampling_loc.shape), dtype=torch.float32, device=dev)
-    if grad_attn is None:
-        grad_attn = torch.empty(tuple(attn_weight.shape), dtype=torch.float32, device=dev)
     sh, st = _host_tables(spatial_shapes, level_start_index)
-    if workspace is None:
-        nbytes = workspace_size(sh.reshape(-1, 2), st, N, S, M, D, Lq, L, P, _dtype_code(value),
-                                MSDA_WORKSPACE_DETERMINISTIC)
-        workspace = torch.empty(max(nbytes, 1), dtype=torch.uint8, device=dev)
+    with _on(stream):
+        if grad_value is None:
+            grad_value = torch.empty((N, S, M, D), dtype=torch.float32, device=dev)
+        if grad_loc is None:
+            grad_loc = torch.empty(tuple(sampling_loc.shape), dtype=torch.float32, device=dev)
+        if grad_attn is None:
+            grad_attn = torch.empty(tuple(attn_weight.shape), dtype=torch.float32, device=dev)
+        if workspace is None:
+            nbytes = workspace_size(sh.reshape(-1, 2), st, N, S, M, D, Lq, L, P, _dtype_code(value),
+                                    MSDA_WORKSPACE_DETERMINISTIC)
+            workspace = torch.empty(max(nbytes, 1), dtype=torch.uint8, device=dev)
     ws_bytes = workspace.numel() * workspace.element_size()
     r = lib().msda_backward_deterministic(_dptr(value), _iptr(sh), _iptr(st), _dptr(sampling_loc),
                                           _dptr(attn_weight), _dptr(grad_out), _dptr(grad_value), _dptr(grad_loc),
@@ -268,7 +302,8 @@ def forward_fused(value, spatial_shapes, level_start_index, ref_points, offsets,
 
     N, S, M, D, Lq, L, P = _fused_dims(value, ref_points, offsets, logits)
     if out is None:
-        out = torch.empty((N, Lq, M * D), dtype=value.dtype, device=value.device)
+        with _on(stream):
+            out = torch.empty((N, Lq, M * D), dtype=value.dtype, device=value.device)
     sh, st = _host_tables(spatial_shapes, level_start_index)
     r = lib().msda_forward_fused(_dptr(value), _iptr(sh), _iptr(st), _dptr(ref_points), _dptr(offsets),
                                  _dptr(logits), _dptr(out), N, S, M, D, Lq, L, P, _dtype_code(value),
@@ -289,21 +324,22 @@ def backward_fused(value, spatial_shapes, level_start_index, ref_points, offsets
 
     N, S, M, D, Lq, L, P = _fused_dims(value, ref_points, offsets, logits)
     dev = value.device
-    if grad_value is None:
-        grad_value = torch.empty((N, S, M, D), dtype=torch.float32, device=dev)
-    if grad_ref is None and want_grad_ref:
-        grad_ref = torch.empty(tuple(ref_points.shape), dtype=torch.float32, device=dev)
-    if grad_offsets is None:
-        grad_offsets = torch.empty(tuple(offsets.shape), dtype=torch.float32, device=dev)
-    if grad_logits is None:
-        grad_logits = torch.empty(tuple(logits.shape), dtype=torch.float32, device=dev)
     sh, st = _host_tables(spatial_shapes, level_start_index)
-    if isinstance(workspace, str):
-        if workspace not in ("auto", "owner"):
-            raise ValueError(f"workspace must be 'auto', 'owner' or a tensor, not {workspace!r}")
-        mode = MSDA_WORKSPACE_PREFERRED if workspace == "auto" else MSDA_WORKSPACE_OWNER
-        nbytes = fused_workspace_size(sh.reshape(-1, 2), st, N, S, M, D, Lq, L, P, _dtype_code(value), mode)
-        workspace = torch.empty(max(nbytes, 1), dtype=torch.uint8, device=dev)
+    with _on(stream):
+        if grad_value is None:
+            grad_value = torch.empty((N, S, M, D), dtype=torch.float32, device=dev)
+        if grad_ref is None and want_grad_ref:
+            grad_ref = torch.empty(tuple(ref_points.shape), dtype=torch.float32, device=dev)
+        if grad_offsets is None:
+            grad_offsets = torch.empty(tuple(offsets.shape), dtype=torch.float32, device=dev)
+        if grad_logits is None:
+            grad_logits = torch.empty(tuple(logits.shape), dtype=torch.float32, device=dev)
+        if isinstance(workspace, str):
+            if workspace not in ("auto", "owner"):
+                raise ValueError(f"workspace must be 'auto', 'owner' or a tensor, not {workspace!r}")
+            mode = MSDA_WORKSPACE_PREFERRED if workspace == "auto" else MSDA_WORKSPACE_OWNER
+            nbytes = fused_workspace_size(sh.reshape(-1, 2), st, N, S, M, D, Lq, L, P, _dtype_code(value), mode)
+            workspace = torch.empty(max(nbytes, 1), dtype=torch.uint8, device=dev)
     ws_bytes = workspace.numel() * workspace.element_size()
     r = lib().msda_backward_fused(_dptr(value), _iptr(sh), _iptr(st), _dptr(ref_points), _dptr(offsets),
                                   _dptr(logits), _dptr(grad_out), _dptr(grad_value),
@@ -324,8 +360,11 @@ def forward_raw(value_ptr: int, shapes: np.ndarray, starts: np.ndarray, loc_ptr:
 def backward_raw(value_ptr: int, shapes: np.ndarray, starts: np.ndarray, loc_ptr: int, attn_ptr: int,
                  gout_ptr: int, gv_ptr: int, gl_ptr: int, ga_ptr: int, ws_ptr: Optional[int], ws_bytes: int,
                  dims: Sequence[int], dtype: int, stream: int, deterministic: bool = False) -> int:
-    """msda_backward (or msda_backward_deterministic) on raw device addresses; returns the status
-    (used by the benchmark loop)."""
+    """msda_backward (msda_backward_deterministic; msda_backward_atomic when ws_ptr is None) on raw
+    device addresses; returns the status (used by the benchmark loop)."""
+    if ws_ptr is None and not deterministic:
+        return lib().msda_backward_atomic(value_ptr, _iptr(shapes), _iptr(starts), loc_ptr, attn_ptr, gout_ptr,
+                                          gv_ptr, gl_ptr, ga_ptr, *dims, dtype, stream)
     fn = lib().msda_backward_deterministic if deterministic else lib().msda_backward
     return fn(value_ptr, _iptr(shapes), _iptr(starts), loc_ptr, attn_ptr, gout_ptr, gv_ptr, gl_ptr, ga_ptr, ws_ptr,
               ws_bytes, *dims, dtype, stream)

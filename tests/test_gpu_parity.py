@@ -292,3 +292,72 @@ def test_adjoint_identities_on_gpu_results():
     r2 = float(np.sum(gpu["grad_attn"].astype(np.float64) * inp.attn.astype(np.float64)))
     scale = float(np.sum(np.abs(inp.grad_out.astype(np.float64) * gpu["out"])))
     assert abs(lhs - r1) <= 1e-5 * scale and abs(lhs - r2) <= 1e-5 * scale
+
+
+def _segment_stream(torch, ptr):
+    for seg in torch.cuda.memory_snapshot():
+        if seg["address"] <= ptr < seg["address"] + seg["total_size"]:
+            return seg["stream"]
+    return None
+
+
+def test_binding_allocates_on_the_call_stream():
+    # outputs and workspaces the binding allocates belong to the stream the kernels run on, so the
+    # caching allocator cannot hand them to other work while the call is still running there
+    import torch
+
+    inp = workloads.random_case(1, 4, 32, ((24, 20), (12, 10)), 4, 2000, "f32", seed=41)
+    d = to_device(inp)
+    say("binding allocations on a stream other than the current one")
+    s = torch.cuda.Stream()
+    torch.cuda.synchronize()
+    assert torch.cuda.current_stream() != s
+    out = msda.forward(d.value, inp.shapes, inp.starts, d.loc, d.attn, stream=s)
+    gv, gl, ga = msda.backward(d.value, inp.shapes, inp.starts, d.loc, d.attn, d.grad_out, workspace="owner",
+                               stream=s)
+    for t in (out, gv, gl, ga):
+        assert _segment_stream(torch, t.data_ptr()) == s.cuda_stream
+    # memory allocated and written on the current stream right away does not disturb the call
+    junk = [torch.full((1 << 22,), float("nan"), device="cuda") for _ in range(4)]
+    s.synchronize()
+    torch.cuda.synchronize()
+    del junk
+    check_parity(inp, gpu={"out": out.cpu().numpy(), "grad_value": gv.cpu().numpy(),
+                           "grad_loc": gl.cpu().numpy(), "grad_attn": ga.cpu().numpy()})
+
+
+def test_release_and_recreate_side_streams():
+    inp = workloads.random_case(1, 4, 32, ((24, 20), (12, 10)), 4, 2000, "f32", seed=42)
+    say("msda_release between backward calls")
+    a = run_gpu(inp, workspace="owner")
+    msda.release()
+    b = run_gpu(inp, workspace="owner")  # the side stream is created again
+    msda.release()
+    msda.release()  # nothing left to release
+    ref = run_oracle(inp)
+    for g in (a, b):
+        check_parity(inp, gpu=g, ref=ref)
+
+
+@pytest.mark.parametrize("name", ["tiny", "detr_decoder", "detr_encoder"])
+def test_atomic_entry_zeroes_then_adds(name):
+    # msda_backward_atomic zeroes grad_value and then adds every corner contribution with fp32
+    # atomics on the same stream: outputs prefilled with NaN show any element that was not zeroed
+    # first or not written, and a stream other than the current one checks the stream handling
+    import torch
+
+    w = workloads.BY_NAME[name]
+    inp = workloads.generate(w)
+    d = to_device(inp)
+    say(f"atomic entry point on NaN-filled outputs, side stream: {name}")
+    s = torch.cuda.Stream()
+    with torch.cuda.stream(s):
+        gv = torch.full(tuple(inp.value.shape), float("nan"), device="cuda")
+        gl = torch.full(tuple(inp.loc.shape), float("nan"), device="cuda")
+        ga = torch.full(tuple(inp.attn.shape), float("nan"), device="cuda")
+    out = msda.forward(d.value, inp.shapes, inp.starts, d.loc, d.attn, stream=s)
+    msda.backward(d.value, inp.shapes, inp.starts, d.loc, d.attn, d.grad_out, gv, gl, ga, workspace=None, stream=s)
+    s.synchronize()
+    gpu = {"out": out.cpu().numpy(), "grad_value": gv.cpu().numpy(), "grad_loc": gl.cpu().numpy(),
+           "grad_attn": ga.cpu().numpy()}
+    check_parity(inp, gpu=gpu, entry="atomic")
