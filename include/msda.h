@@ -144,6 +144,31 @@ msda_status_t msda_backward_atomic(const void* value, const int64_t* spatial_sha
                                    int64_t D, int64_t Lq, int64_t L, int64_t P, int dtype, void* stream);
 
 /*
+ * For callers that cannot allocate device memory (code under HIP graph capture, tight serving
+ * loops, harnesses that forbid hipMalloc): msda_backward without a workspace argument and without
+ * allocating anything. The owner-computes grad_value takes its scratch from a static device array
+ * of MSDA_NOALLOC_SCRATCH_BYTES that the library holds on every GPU it runs on until the process
+ * ends; problems msda_backward would run without a workspace use fp32 atomics as it does. Results
+ * are those of msda_backward. All work runs on `stream` alone (no side stream). No hipMalloc,
+ * hipFree or allocating runtime call is made; the first call on a device looks up the array's
+ * address there.
+ *
+ * Every call on one GPU shares that GPU's array: calls whose work overlaps on one GPU (on
+ * different streams, or from different threads without ordering) race and give wrong grad_value.
+ * The array keeps the last call's contents; everything that must start at zero is cleared by the
+ * call itself. A problem whose workspace (msda_backward_workspace_size with
+ * MSDA_WORKSPACE_PREFERRED) exceeds MSDA_NOALLOC_SCRATCH_BYTES is MSDA_ERROR_NOT_SUPPORTED
+ * (the DETR-encoder shape needs 82 MiB; the BEVFormer and Swin-feature shapes need more).
+ * Pointer alignment and N*Lq == 0 as for msda_backward.
+ */
+#define MSDA_NOALLOC_SCRATCH_BYTES ((size_t)128 << 20)
+msda_status_t msda_backward_noalloc(const void* value, const int64_t* spatial_shapes,
+                                    const int64_t* level_start_index, const float* sampling_loc,
+                                    const float* attn_weight, const void* grad_out, float* grad_value,
+                                    float* grad_loc, float* grad_attn, int64_t N, int64_t S, int64_t M,
+                                    int64_t D, int64_t Lq, int64_t L, int64_t P, int dtype, void* stream);
+
+/*
  * Backward pass with a bitwise reproducible grad_value: the same as msda_backward (same arguments,
  * layouts, ownership and results within rounding), except that every grad_value element is summed
  * in an order fixed by the inputs alone, so repeated calls on the same inputs give the same bits

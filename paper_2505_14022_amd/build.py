@@ -13,7 +13,8 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 LIB_DIR = os.path.join(PKG, "_lib")
 LIB_PATH = os.path.join(LIB_DIR, "libmsda.so")
-SOURCES = ["msda_api.cpp", "msda_fwd.hip", "msda_bwd.hip", "msda_bwd_value.hip", "msda_prologue.hip"]
+SOURCES = ["msda_api.cpp", "msda_fwd.hip", "msda_bwd.hip", "msda_bwd_value.hip", "msda_prologue.hip",
+           "msda_noalloc.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"

@@ -10,6 +10,8 @@
 #include "msda.h"
 #include "msda_internal.h"
 
+static_assert(MSDA_NOALLOC_SCRATCH_BYTES == msda::kStaticScratchBytes, "static scratch size in msda.h");
+
 namespace {
 
 thread_local char g_last_error[512] = "";
@@ -424,6 +426,47 @@ msda_status_t msda_backward_atomic(const void* value, const int64_t* spatial_sha
     Sampling smp = {sampling_loc, attn_weight, grad_loc, grad_attn};
     return backward_body(value, spatial_shapes, level_start_index, grad_out, grad_value, smp, nullptr, nullptr, N,
                          S, M, D, Lq, L, P, dtype, (hipStream_t)stream);
+}
+
+msda_status_t msda_backward_noalloc(const void* value, const int64_t* spatial_shapes,
+                                    const int64_t* level_start_index, const float* sampling_loc,
+                                    const float* attn_weight, const void* grad_out, float* grad_value,
+                                    float* grad_loc, float* grad_attn, int64_t N, int64_t S, int64_t M, int64_t D,
+                                    int64_t Lq, int64_t L, int64_t P, int dtype, void* stream) {
+    msda_status_t st = check_problem(spatial_shapes, level_start_index, N, S, M, D, Lq, L, P, dtype);
+    if (st != MSDA_SUCCESS) return st;
+    if (N == 0) return ok();
+    if (Lq > 0) {
+        if (!sampling_loc || !attn_weight || !grad_loc || !grad_attn)
+            return fail(MSDA_ERROR_INVALID_VALUE,
+                        "value, sampling_loc, attn_weight, grad_out, grad_loc and grad_attn must be non-null");
+        if (!aligned(sampling_loc, 8) || !aligned(grad_loc, 8) || !aligned(attn_weight, 4) || !aligned(grad_attn, 4))
+            return fail(MSDA_ERROR_INVALID_VALUE,
+                        "misaligned pointer: value and grad_out need 16 bytes, sampling_loc and grad_loc 8, "
+                        "attn_weight and grad_attn 4");
+    }
+    // the workspace msda_backward would prefer: none (fp32 atomics) for small or sparse problems
+    size_t need = 0;
+    if (Lq > 0) {
+        st = msda_backward_workspace_size(spatial_shapes, level_start_index, N, S, M, D, Lq, L, P, dtype,
+                                          MSDA_WORKSPACE_PREFERRED, &need);
+        if (st != MSDA_SUCCESS) return st;
+    }
+    if (need > msda::kStaticScratchBytes)
+        return fail(MSDA_ERROR_NOT_SUPPORTED,
+                    "this problem needs %zu bytes of scratch; the static scratch of msda_backward_noalloc holds %zu "
+                    "(use msda_backward with a workspace)", need, msda::kStaticScratchBytes);
+    void* ws = nullptr;
+    if (need > 0) {
+        const int dev = stream_device((hipStream_t)stream);
+        hipError_t e = dev < 0 ? hipErrorInvalidDevice : msda::static_scratch(dev, &ws);
+        if (e != hipSuccess)
+            return fail(MSDA_ERROR_LAUNCH_FAILED, "static scratch address: %s", hipGetErrorString(e));
+    }
+    Sampling smp = {sampling_loc, attn_weight, grad_loc, grad_attn};
+    // one stream only: no library stream or event is created or used
+    return backward_body(value, spatial_shapes, level_start_index, grad_out, grad_value, smp, nullptr, ws, N, S, M,
+                         D, Lq, L, P, dtype, (hipStream_t)stream, false, true);
 }
 
 msda_status_t msda_backward_deterministic(const void* value, const int64_t* spatial_shapes,

@@ -25,6 +25,8 @@ constexpr int kChunkRecords = 512;   // records folded by one accumulate work it
 constexpr int kCountQueries = 4096;  // samples per workgroup in the counting / scatter passes
 constexpr int kScanTiles = 256;      // tiles per workgroup in the scan passes (one per thread)
 constexpr int kAtomicMaxSamples = 16384;  // problems this small take the atomic grad_value path
+// Bytes of the static device scratch of msda_backward_noalloc (per GPU, held until the process ends).
+constexpr size_t kStaticScratchBytes = size_t(128) << 20;
 
 // Everything one launch needs, passed by value as the kernel argument.
 struct Params {
@@ -106,6 +108,10 @@ hipError_t launch_binned_reset(const Params& p, hipStream_t stream);
 // grad_value by binning samples per destination tile and accumulating each tile once.
 hipError_t launch_backward_value_binned(const Params& p, msda_dtype_t dtype, hipStream_t stream);
 hipError_t launch_zero(float* ptr, int64_t n, hipStream_t stream);
+
+// Device address of the static scratch array (kStaticScratchBytes) on `device`, looked up on the
+// first call for that device; no allocation.
+hipError_t static_scratch(int device, void** ptr);
 
 // True when fp32 atomics are expected to beat the binned grad_value path (sparse or small problems).
 bool prefer_atomic(const Params& p);

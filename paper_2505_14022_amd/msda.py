@@ -29,7 +29,8 @@ MSDA_WORKSPACE_DETERMINISTIC = 2
 EXPORTED = ["msda_check_args", "msda_forward", "msda_backward", "msda_backward_atomic",
             "msda_backward_deterministic", "msda_backward_workspace_size",
             "msda_forward_fused", "msda_backward_fused_workspace_size", "msda_backward_fused",
-            "msda_status_string", "msda_last_error", "msda_version", "msda_release"]
+            "msda_status_string", "msda_last_error", "msda_version", "msda_release", "msda_backward_noalloc"]
+MSDA_NOALLOC_SCRATCH_BYTES = 128 << 20
 
 
 class MsdaError(RuntimeError):
@@ -58,6 +59,8 @@ def lib():
         L.msda_backward.restype = ctypes.c_int
         L.msda_backward_atomic.argtypes = [vp, ip, ip, vp, vp, vp, vp, vp, vp] + [i64] * 7 + [ctypes.c_int, vp]
         L.msda_backward_atomic.restype = ctypes.c_int
+        L.msda_backward_noalloc.argtypes = L.msda_backward_atomic.argtypes
+        L.msda_backward_noalloc.restype = ctypes.c_int
         L.msda_backward_deterministic.argtypes = L.msda_backward.argtypes
         L.msda_backward_deterministic.restype = ctypes.c_int
         L.msda_backward_workspace_size.argtypes = [ip, ip] + [i64] * 7 + [ctypes.c_int, ctypes.c_int,
@@ -238,6 +241,19 @@ def backward(value, spatial_shapes, level_start_index, sampling_loc, attn_weight
                             _dptr(grad_out), _dptr(grad_value), _dptr(grad_loc), _dptr(grad_attn), ws_ptr, ws_bytes,
                             N, S, M, D, Lq, L, P, _dtype_code(value), _stream(stream))
     _raise(r, "msda_backward")
+    return grad_value, grad_loc, grad_attn
+
+
+def backward_noalloc(value, spatial_shapes, level_start_index, sampling_loc, attn_weight, grad_out,
+                     grad_value, grad_loc, grad_attn, stream=None):
+    """msda_backward_noalloc into caller-allocated outputs: the library allocates nothing (its
+    owner-computes scratch is a static device array of MSDA_NOALLOC_SCRATCH_BYTES per GPU)."""
+    N, S, M, D, Lq, L, P = _dims(value, sampling_loc)
+    sh, st = _host_tables(spatial_shapes, level_start_index)
+    r = lib().msda_backward_noalloc(_dptr(value), _iptr(sh), _iptr(st), _dptr(sampling_loc), _dptr(attn_weight),
+                                    _dptr(grad_out), _dptr(grad_value), _dptr(grad_loc), _dptr(grad_attn),
+                                    N, S, M, D, Lq, L, P, _dtype_code(value), _stream(stream))
+    _raise(r, "msda_backward_noalloc")
     return grad_value, grad_loc, grad_attn
 
 

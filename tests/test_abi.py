@@ -297,3 +297,17 @@ def test_backward_without_workspace_is_explicit(L, no_gpu):
 def test_release_without_side_streams_succeeds(L, no_gpu):
     # nothing was created on a machine without a GPU: releasing is a no-op that succeeds
     assert L.msda_release() == msda.MSDA_SUCCESS
+
+
+def test_noalloc_rejects_beyond_its_scratch_on_the_host(L, no_gpu):
+    # the size limit is checked before any device is touched
+    w = workloads.BY_NAME["bev_sca"]
+    sh, st = w.shapes_array(), w.starts()
+    ip = ctypes.POINTER(ctypes.c_int64)
+    r = L.msda_backward_noalloc(0x1000, sh.ctypes.data_as(ip), st.ctypes.data_as(ip), 0x2000, 0x3000, 0x4000,
+                                0x5000, 0x6000, 0x7000, w.N, w.S, w.M, w.D, w.Lq, w.L, w.P, msda.MSDA_F32, None)
+    assert r == msda.MSDA_ERROR_NOT_SUPPORTED and "scratch" in msda.last_error()
+    # the headline DETR-encoder shape fits the static scratch
+    d = workloads.BY_NAME["detr_encoder"]
+    need = msda.workspace_size(d.shapes_array(), d.starts(), d.N, d.S, d.M, d.D, d.Lq, d.L, d.P, msda.MSDA_F32)
+    assert 0 < need <= msda.MSDA_NOALLOC_SCRATCH_BYTES
