@@ -181,6 +181,8 @@ def main():
     ap.add_argument("--no-compulsory", action="store_true", help="skip counting touched rows (faster)")
     ap.add_argument("--atomic-grad-value", action="store_true",
                     help="pass no workspace, so msda_backward accumulates grad_value with fp32 atomics")
+    ap.add_argument("--owner-grad-value", action="store_true",
+                    help="pass the owner-computes workspace even where the library prefers atomics")
     ap.add_argument("--deterministic", action="store_true",
                     help="time msda_backward_deterministic (bitwise reproducible grad_value) as the backward")
     ap.add_argument("--fused", action="store_true",
@@ -254,7 +256,8 @@ def main():
         loc, attn = dev_in(inp.loc), dev_in(inp.attn)
         gl = torch.empty(tuple(loc.shape), dtype=torch.float32, device=dev)
         ga = torch.empty(tuple(attn.shape), dtype=torch.float32, device=dev)
-        ws_mode = msda.MSDA_WORKSPACE_DETERMINISTIC if args.deterministic else msda.MSDA_WORKSPACE_PREFERRED
+        ws_mode = (msda.MSDA_WORKSPACE_DETERMINISTIC if args.deterministic else
+                   msda.MSDA_WORKSPACE_OWNER if args.owner_grad_value else msda.MSDA_WORKSPACE_PREFERRED)
         ws_bytes = 0 if args.atomic_grad_value else msda.workspace_size(inp.shapes, inp.starts, *dims, dt, ws_mode)
         binned_bytes = ws_bytes
         ws = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device=dev)

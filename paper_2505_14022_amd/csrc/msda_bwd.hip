@@ -20,6 +20,8 @@ namespace {
 #define MSDA_BWD_UNROLL 1
 #endif
 constexpr int kBwdU = MSDA_BWD_UNROLL;
+// grad_out floats of one wave's queries staged in LDS by the atomic variant (PPW * D at most)
+constexpr int kAtomicRowFloats = 512;
 
 
 // Sums each of the four corner dot products over the query's LPP lanes and stores the four totals
@@ -55,6 +57,12 @@ __global__ __launch_bounds__(kBlock) void bwd_kernel(Params p) {
     __shared__ int s_lvl[3 * kMaxLevels];
     __shared__ int4 s_off[kWaves][kMaxItems];
     __shared__ float4 s_x[kWaves][kMaxItems];  // {a, lh, lw, -} of each sample
+    // ATOMIC: the wave's grad_out rows (one per query), for the coalesced atomics below, and the
+    // corner sums of the chunk's samples, kept apart from their offsets, which the atomics read
+    // after all sums are formed
+    __shared__ float s_g[kWaves][ATOMIC ? kAtomicRowFloats : 1];
+    __shared__ int4 s_sum_atomic[kWaves][ATOMIC ? kMaxItems : 1];
+    int4* const s_sum = ATOMIC ? &s_sum_atomic[0][0] : &s_off[0][0];  // [kWaves][kMaxItems] when used
     load_levels(p, s_lvl);
 
     Tile t;
@@ -76,6 +84,17 @@ __global__ __launch_bounds__(kBlock) void bwd_kernel(Params p) {
 #pragma unroll
     for (int i = 0; i < VEC; ++i) g_row[i] = 0.f;
     if (one_pass && sub * VEC < p.D) Row<T, VEC>::load_ptr(g_row, gout + gout_row + sub * VEC);
+    // ATOMIC with one row piece per lane: the grad_value atomics of a sample are regrouped so that
+    // each instruction's lanes cover whole rows (32 lanes = one 128-byte row at D = 32) instead of
+    // LPP-lane pieces of eight rows; the memory side retires them as half as many requests
+    const bool coalesced = ATOMIC && p.D == LPP * VEC && PPW * p.D <= kAtomicRowFloats;
+    if constexpr (ATOMIC) {
+        if (coalesced && sub * VEC < p.D) {
+#pragma unroll
+            for (int i = 0; i < VEC; ++i)
+                if (sub * VEC + i < p.D) s_g[wave][ps * p.D + sub * VEC + i] = g_row[i];
+        }
+    }
 
     for (int k0 = 0; k0 < K; k0 += KC) {
         const int kn = K - k0 < KC ? K - k0 : KC;
@@ -89,19 +108,22 @@ __global__ __launch_bounds__(kBlock) void bwd_kernel(Params p) {
         }
         wave_lds_sync();
         const int base = ps * kn;
-        const bool general = ATOMIC || !one_pass;
+        const bool general = (ATOMIC && !coalesced) || !one_pass;
         if (!general) {
             // the query's channels are one row piece per lane: no channel loop around the loads
-            // (a second register set with the next sample's rows in flight was slower at the
-            // Swin-feature shape and tied elsewhere)
             const uint32_t cb = (uint32_t)(sub * VEC) << Row<T, VEC>::kShift;
-            for (int kk = 0; kk < kn; ++kk) {
-                const int4 o = s_off[wave][base + kk];
-                float v[4][VEC];
+            auto load_corners = [&](float (&v)[4][VEC], int4 o) {
                 Row<T, VEC>::load(v[0], vr, ((uint32_t)o.x << Row<T, VEC>::kShift) + cb);
                 Row<T, VEC>::load(v[1], vr, ((uint32_t)o.y << Row<T, VEC>::kShift) + cb);
                 Row<T, VEC>::load(v[2], vr, ((uint32_t)o.z << Row<T, VEC>::kShift) + cb);
                 Row<T, VEC>::load(v[3], vr, ((uint32_t)o.w << Row<T, VEC>::kShift) + cb);
+            };
+            // the four corner dot products G_c = <g, v_c>, summed over the query's lanes into slot kk
+            // (a second register set with the next sample's rows in flight was slower at the
+            // Swin-feature shape and tied elsewhere)
+            for (int kk = 0; kk < kn; ++kk) {
+                float v[4][VEC];
+                load_corners(v, s_off[wave][base + kk]);
                 float G[4];
 #pragma unroll
                 for (int c = 0; c < 4; ++c) {
@@ -109,8 +131,34 @@ __global__ __launch_bounds__(kBlock) void bwd_kernel(Params p) {
 #pragma unroll
                     for (int i = 0; i < VEC; ++i) G[c] += g_row[i] * v[c][i];
                 }
-                // the sums overwrite only this sample's (already read) slot
-                store_corner_sums<LPP>(G, sub, &s_off[wave][base + kk]);
+                // the sums overwrite only this sample's (already read) slot, or go to s_sum
+                store_corner_sums<LPP>(G, sub, &s_sum[wave * kMaxItems + base + kk]);
+            }
+            if constexpr (ATOMIC) {
+                // grad_value[corner row] += a * w_corner * g for every (query, sample, corner) of
+                // the chunk, after its gathers: flat index f = 64 j + lane of instruction j runs
+                // over (query, corner, channel), so consecutive lanes add consecutive channels of one
+                // row (32 lanes = one 128-byte row at D = 32), half as many memory-side requests as
+                // pieces of eight rows. No load follows them in the chunk, so the wave never waits
+                // for them to complete.
+                constexpr int DC = LPP * VEC;  // = D here (a power of two)
+                constexpr int kPerQ = 4 * DC, kTotal = PPW * kPerQ;
+                static_assert(kTotal % 64 == 0, "whole instructions");
+                wave_lds_sync();
+                for (int kk = 0; kk < kn; ++kk) {
+#pragma unroll
+                    for (int j = 0; j < kTotal / 64; ++j) {
+                        const int f = 64 * j + lane;
+                        const int qq = f / kPerQ, r = f % kPerQ, c = r / DC, ch = r % DC;
+                        const int slot = qq * kn + kk;
+                        const int off = reinterpret_cast<const int*>(&s_off[wave][slot])[c];
+                        const float4 x = s_x[wave][slot];
+                        const float wr = (c & 2) ? x.y : 1.f - x.y, wc = (c & 1) ? x.z : 1.f - x.z;
+                        const float add = (x.x * (wr * wc)) * s_g[wave][qq * DC + ch];
+                        __builtin_amdgcn_raw_ptr_buffer_atomic_fadd_f32(
+                            add, gr, ((uint32_t)off << 2) + ((uint32_t)ch << 2), 0, 0);
+                    }
+                }
             }
         }
         // kBwdU samples at a time: their 4 * kBwdU corner rows are loaded together, then the sums
@@ -192,13 +240,13 @@ __global__ __launch_bounds__(kBlock) void bwd_kernel(Params p) {
             for (int u = 0; u < kBwdU; ++u)
 #pragma unroll
                 for (int c = 0; c < 4; ++c) G[u][c] = group_sum<LPP>(G[u][c]);
-            // the four sums replace the sample's corner offsets in LDS (every lane has read them:
-            // a wave's LDS operations complete in order)
+            // the four sums replace the sample's corner offsets in LDS, or go to s_sum (every lane
+            // has read the offsets: a wave's LDS operations complete in order)
             if (sub == 0) {
 #pragma unroll
                 for (int u = 0; u < kBwdU; ++u)
                     if (kk0 + u < kn)
-                        s_off[wave][base + kk0 + u] =
+                        s_sum[wave * kMaxItems + base + kk0 + u] =
                             make_int4(__builtin_bit_cast(int, G[u][0]), __builtin_bit_cast(int, G[u][1]),
                                       __builtin_bit_cast(int, G[u][2]), __builtin_bit_cast(int, G[u][3]));
             }
@@ -210,7 +258,7 @@ __global__ __launch_bounds__(kBlock) void bwd_kernel(Params p) {
             const int jq = j / kn, jk = j - jq * kn;
             const int q = t.q0 + jq;
             if (q < p.Lq) {
-                const int4 gi = s_off[wave][j];
+                const int4 gi = s_sum[wave * kMaxItems + j];
                 const float G0 = __builtin_bit_cast(float, gi.x), G1 = __builtin_bit_cast(float, gi.y);
                 const float G2 = __builtin_bit_cast(float, gi.z), G3 = __builtin_bit_cast(float, gi.w);
                 const float4 x = s_x[wave][j];

@@ -318,16 +318,22 @@ inline int pick_lpp(int D, int vec) {
     return lpp;
 }
 
-// Launches KernelT<T, VEC, lpp>::fn() over (slab, query chunk) workgroups of kBlock lanes.
+// Launches KernelT<T, VEC, lpp>::fn() over (slab, query chunk) workgroups of kBlock lanes, or of
+// one wave each when that many workgroups would leave CUs idle: a wave's work does not depend on
+// the other waves of its workgroup, and at the DETR-decoder shape (160 four-wave workgroups)
+// one-wave workgroups spread the grad_value atomics over all CUs.
+constexpr int kSmallGrid = 1024;
 template <template <typename, int, int> class KernelT, typename T, int VEC>
 hipError_t launch_lpp(Params p, int lpp, hipStream_t stream) {
     auto go = [&](auto kernel, int ppw) -> hipError_t {
-        p.q_per_block = kWaves * ppw;
+        const int64_t chunks4 = (p.Lq + kWaves * ppw - 1) / (kWaves * ppw);
+        const int waves = (int64_t)p.n_batch * p.M * chunks4 < kSmallGrid ? 1 : kWaves;
+        p.q_per_block = waves * ppw;
         p.chunks = (p.Lq + p.q_per_block - 1) / p.q_per_block;
         p.num_blocks = p.n_batch * p.M * p.chunks;
         if (p.num_blocks == 0) return hipSuccess;
         const int grid = (p.num_blocks + 7) / 8 * 8;
-        hipLaunchKernelGGL(kernel, dim3(grid), dim3(kBlock), 0, stream, p);
+        hipLaunchKernelGGL(kernel, dim3(grid), dim3(64 * waves), 0, stream, p);
         return hipGetLastError();
     };
     switch (lpp) {

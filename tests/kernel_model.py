@@ -29,6 +29,8 @@ import numpy as np
 MAX_LAUNCH_ELEMS = 1 << 29  # per-launch element limit; also the off-map sentinel offset
 MAX_INDEX = (1 << 31) - 1
 WAVES_PER_BLOCK = 4
+SMALL_GRID = 1024        # below this many four-wave workgroups, workgroups of one wave are launched
+ATOMIC_ROW_FLOATS = 512  # grad_out floats of one wave staged for the row-coalesced atomics
 U32 = 1 << 32
 
 
@@ -74,6 +76,7 @@ class Launch:
     vec: int
     lpp: int
     ppw: int
+    waves: int
     q_per_block: int
     chunks: int
     num_blocks: int
@@ -89,14 +92,16 @@ def launches(N, S, M, D, Lq, L, P, es):
     vec = pick_vec(D, es)
     lpp = pick_lpp(D, vec)
     ppw = 64 // lpp
-    qpb = WAVES_PER_BLOCK * ppw
     out = []
     for n0 in range(0, N, nb):
         cnt = min(nb, N - n0)
+        chunks4 = (Lq + WAVES_PER_BLOCK * ppw - 1) // (WAVES_PER_BLOCK * ppw)
+        waves = 1 if cnt * M * chunks4 < SMALL_GRID else WAVES_PER_BLOCK
+        qpb = waves * ppw
         chunks = (Lq + qpb - 1) // qpb
         num_blocks = cnt * M * chunks
         grid = (num_blocks + 7) // 8 * 8
-        out.append(Launch(n0, cnt, vec, lpp, ppw, qpb, chunks, num_blocks, grid))
+        out.append(Launch(n0, cnt, vec, lpp, ppw, waves, qpb, chunks, num_blocks, grid))
     return out
 
 
@@ -114,7 +119,7 @@ def wave_queries(ln: Launch, M: int):
     w = w[w < ln.num_blocks]
     slab, chunk = w // ln.chunks, w % ln.chunks
     n, m = slab // M, slab % M
-    wave = np.arange(WAVES_PER_BLOCK, dtype=np.int64)
+    wave = np.arange(ln.waves, dtype=np.int64)
     ps = np.arange(ln.ppw, dtype=np.int64)
     q = (chunk[:, None, None] * ln.q_per_block + wave[None, :, None] * ln.ppw + ps[None, None, :])
     shp = q.shape
@@ -122,10 +127,34 @@ def wave_queries(ln: Launch, M: int):
             q.ravel())
 
 
+def coalesced_atomics(D: int, vec: int, lpp: int) -> bool:
+    """Whether the atomics take the row-coalesced mapping (one row piece per lane, PPW*D staged)."""
+    return D == lpp * vec and (64 // lpp) * D <= ATOMIC_ROW_FLOATS
+
+
+def coalesced_map(D: int, vec: int, lpp: int):
+    """The row-coalesced atomics: instruction j, lane L add flat index f = 64 j + L of
+    (query slot, corner, channel) = (f / 4D, (f / D) % 4, f % D); checked to cover every
+    (query slot, corner, channel) of a wave exactly once, 32 consecutive lanes on one row."""
+    ppw = 64 // lpp
+    total = ppw * 4 * D
+    _check(total % 64 == 0, "coalesced atomics need whole instructions")
+    seen = np.zeros((ppw, 4, D), dtype=np.int64)
+    for j in range(total // 64):
+        f = 64 * j + np.arange(64)
+        qq, r = f // (4 * D), f % (4 * D)
+        c, ch = r // D, r % D
+        np.add.at(seen, (qq, c, ch), 1)
+    _check(np.all(seen == 1), f"coalesced atomics do not cover (query, corner, channel) once at D={D}")
+    return total // 64
+
+
 def lane_channel_maps(D: int, vec: int, lpp: int):
     """Channels read by value-row loads (lane sub, pass c0: [c0 + sub*vec, +vec)) and channels
-    added by the atomics (lane sub, pass c0, element i: c0 + sub + lpp*i), each checked to cover
-    [0, D) exactly once."""
+    added by the atomics (lane sub, pass c0, element i: c0 + sub + lpp*i; or the row-coalesced
+    mapping), each checked to cover [0, D) exactly once."""
+    if coalesced_atomics(D, vec, lpp):
+        coalesced_map(D, vec, lpp)
     loads, atom = [], []
     for c0 in range(0, D, lpp * vec):
         for sub in range(lpp):

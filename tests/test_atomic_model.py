@@ -48,9 +48,9 @@ def test_small_cases(case):
 
 def test_tiny_workload_with_tail_queries():
     stats = _compare(workloads.generate(workloads.BY_NAME["tiny"]))
-    # Lq = 16 queries in a 4-wave workgroup of 32-query waves: most slots are past Lq and must
-    # drop every access
-    assert stats["tail_slots"] > stats["sample_slots"]
+    # Lq = 16 queries in one-wave workgroups of 32-query waves: half of the slots are past Lq and
+    # must drop every access
+    assert stats["tail_slots"] >= stats["sample_slots"] > 0
 
 
 @pytest.mark.parametrize("name", ["detr_decoder", "detr_encoder"])
