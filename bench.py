@@ -35,6 +35,8 @@ sys.path.insert(0, ROOT)
 from paper_2505_14022_amd import msda, workloads  # noqa: E402
 
 HBM_PEAK_GBS = 8000.0
+# measured beside the headline workload in the same run (BEVFormer spatial / temporal attention)
+SECONDARY = ("bev_sca", "bev_tsa_f16")
 PROFILES = os.path.join(ROOT, "profiles")
 SOURCE_DIRS = [os.path.join(ROOT, "paper_2505_14022_amd", "csrc"), os.path.join(ROOT, "include")]
 
@@ -171,49 +173,9 @@ def cpu_baseline(inp, budget_s: float = 10.0, fused: bool = False):
                       f"workload ({inp.w.samples} samples each), fp64 oracle, OpenMP threads={th}"}
 
 
-def main():
-    ap = argparse.ArgumentParser()
-    ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=100)
-    ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--workload", default="detr_encoder", choices=sorted(workloads.BY_NAME))
-    ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--no-compulsory", action="store_true", help="skip counting touched rows (faster)")
-    ap.add_argument("--atomic-grad-value", action="store_true",
-                    help="pass no workspace, so msda_backward accumulates grad_value with fp32 atomics")
-    ap.add_argument("--owner-grad-value", action="store_true",
-                    help="pass the owner-computes workspace even where the library prefers atomics")
-    ap.add_argument("--deterministic", action="store_true",
-                    help="time msda_backward_deterministic (bitwise reproducible grad_value) as the backward")
-    ap.add_argument("--fused", action="store_true",
-                    help="time msda_forward_fused + msda_backward_fused (inputs: reference points, pixel offsets, "
-                         "logits)")
-    ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
-                    help="instead of the benchmark, copy a MIB-mebibyte fp32 buffer 5 times (a plain copy kernel of "
-                         "known size, used to scale FETCH_SIZE / WRITE_SIZE counters)")
-    args = ap.parse_args()
-    if args.gpus != 1:
-        print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported (MSDA shards over batch "
-              f"and heads with no exchange, so the per-GPU figure is the one-GPU figure)", file=sys.stderr)
-        sys.exit(2)
-
-    import torch
-
-    if not torch.cuda.is_available():
-        print("no GPU visible", file=sys.stderr)
-        sys.exit(1)
-    if args.copy_calibration:
-        n = args.copy_calibration << 18  # fp32 elements
-        src = torch.ones(n, device="cuda")
-        dst = torch.empty_like(src)
-        for _ in range(5):
-            dst.copy_(src)
-        torch.cuda.synchronize()
-        print(json.dumps({"copy_calibration_bytes_per_direction": n * 4, "copies": 5}))
-        return
-    msda.lib()
-
-    w = workloads.BY_NAME[args.workload]
+def measure(torch, w, args, steps, warmup, compulsory=True, traffic=True):
+    """Time `steps` forward + backward steps of workload `w` after `warmup` untimed ones; returns the
+    result dict (without the CPU baseline) and the inputs."""
     print(f"[bench] generating {w.name}", file=sys.stderr, flush=True)
     inp = workloads.generate_fused(w) if args.fused else workloads.generate(w)
     dev = torch.device("cuda:0")
@@ -275,13 +237,13 @@ def main():
             if r:
                 raise msda.MsdaError(r, "msda_backward", msda.last_error())
 
-    print(f"[bench] warmup {args.warmup}", file=sys.stderr, flush=True)
-    for _ in range(args.warmup):
+    print(f"[bench] warmup {warmup}", file=sys.stderr, flush=True)
+    for _ in range(warmup):
         fwd()
         bwd()
     torch.cuda.synchronize()
 
-    K = args.steps
+    K = steps
     ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(K)]
     print(f"[bench] timing {K} steps", file=sys.stderr, flush=True)
     torch.cuda.synchronize()
@@ -305,7 +267,7 @@ def main():
         "unit": "Gsamples/s",
         "n_gpus": 1,
         "steps": K,
-        "warmup": args.warmup,
+        "warmup": warmup,
         "ms_per_step": round(step_ms, 5),
         "higher_is_better": True,
         "scaling": "weak",
@@ -324,7 +286,7 @@ def main():
                             "owner-computes (binned)") if binned_bytes else "atomic",
         "workspace_bytes": int(ws_bytes),
     }
-    if not args.no_compulsory:
+    if compulsory:
         print("[bench] counting compulsory bytes", file=sys.stderr, flush=True)
         fb, bb, rows, gathered = compulsory_bytes(inp, args.fused)
         bwd_s = float(bwd_ms.mean()) / 1e3
@@ -334,7 +296,7 @@ def main():
         bname = "msda_backward_fused" if args.fused else "msda_backward"
         res["roofline"] = {"bound": "hbm", "kernel": f"{bname} (all of its kernels, one call)",
                            "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                           "frac": round(achieved / HBM_PEAK_GBS, 5), "traffic": None if args.fused else measured_traffic(w.name),
+                           "frac": round(achieved / HBM_PEAK_GBS, 5), "traffic": None if (args.fused or not traffic) else measured_traffic(w.name),
                            "algorithmic_bytes": int(bb), "launch_ms": round(float(bwd_ms.mean()), 5),
                            "copy_peak": round(copy_gbs, 1), "frac_of_copy_peak": round(achieved / copy_gbs, 5)}
         res["fwd_roofline"] = {"bound": "hbm", "kernel": "msda_forward_fused (fwd_kernel)" if args.fused else
@@ -348,6 +310,71 @@ def main():
                                "gathered_TBps": round(gathered / fwd_s / 1e12, 3)}
         res["step_hbm_frac"] = round((fb + bb) / (step_ms / 1e3) / 1e9 / HBM_PEAK_GBS, 5)
         res["touched_value_rows"] = rows
+    return res, inp
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default="detr_encoder", choices=sorted(workloads.BY_NAME))
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-compulsory", action="store_true", help="skip counting touched rows (faster)")
+    ap.add_argument("--no-secondary", action="store_true", help="skip the BEVFormer-shaped lines")
+    ap.add_argument("--atomic-grad-value", action="store_true",
+                    help="pass no workspace, so msda_backward accumulates grad_value with fp32 atomics")
+    ap.add_argument("--owner-grad-value", action="store_true",
+                    help="pass the owner-computes workspace even where the library prefers atomics")
+    ap.add_argument("--deterministic", action="store_true",
+                    help="time msda_backward_deterministic (bitwise reproducible grad_value) as the backward")
+    ap.add_argument("--fused", action="store_true",
+                    help="time msda_forward_fused + msda_backward_fused (inputs: reference points, pixel offsets, "
+                         "logits)")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                    help="instead of the benchmark, copy a MIB-mebibyte fp32 buffer 5 times (a plain copy kernel of "
+                         "known size, used to scale FETCH_SIZE / WRITE_SIZE counters)")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported (MSDA shards over batch "
+              f"and heads with no exchange, so the per-GPU figure is the one-GPU figure)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    if not torch.cuda.is_available():
+        print("no GPU visible", file=sys.stderr)
+        sys.exit(1)
+    if args.copy_calibration:
+        n = args.copy_calibration << 18  # fp32 elements
+        src = torch.ones(n, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(5):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_calibration_bytes_per_direction": n * 4, "copies": 5}))
+        return
+    msda.lib()
+    w = workloads.BY_NAME[args.workload]
+    res, inp = measure(torch, w, args, args.steps, args.warmup, compulsory=not args.no_compulsory)
+    if not args.no_secondary and not args.fused and not args.deterministic:
+        # BEVFormer-shaped workloads beside the headline one: step time, rate and the backward's
+        # roofline fraction, fewer steps and no CPU baseline
+        res["secondary"] = {}
+        for name in SECONDARY:
+            if name == w.name:
+                continue
+            r2, _ = measure(torch, workloads.BY_NAME[name], args, 20, 5, compulsory=not args.no_compulsory,
+                            traffic=False)
+            keep = {"step_ms": r2["ms_per_step"], "Gsamples_per_s": r2["value"], "fwd_ms": r2["fwd_ms_mean"],
+                    "bwd_ms": r2["bwd_ms_mean"], "dtype": r2["dtype"], "samples_per_step": r2["config"]["samples_per_step"],
+                    "grad_value_path": r2["grad_value_path"], "steps": 20, "warmup": 5}
+            if "roofline" in r2:
+                keep["bwd_roofline_frac"] = r2["roofline"]["frac"]
+                keep["bwd_algorithmic_bytes"] = r2["roofline"]["algorithmic_bytes"]
+                keep["fwd_roofline_frac"] = r2["fwd_roofline"]["frac"]
+                keep["step_hbm_frac"] = r2["step_hbm_frac"]
+            res["secondary"][name] = keep
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle", file=sys.stderr, flush=True)
         res["cpu_baseline"] = cpu_baseline(inp, fused=args.fused)
