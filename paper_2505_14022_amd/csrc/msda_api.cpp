@@ -216,6 +216,9 @@ msda_status_t backward_body(const void* value, const int64_t* shapes, const int6
     // caller's stream's device; the lock spans every fork and join this call enqueues
     std::unique_lock<std::mutex> side_lock(g_side_mutex, std::defer_lock);
     SideStream* side = nullptr;
+#ifdef MSDA_ABLATE_ONE_STREAM
+    one_stream = true;
+#endif
     if (binned && !one_stream) {
         side_lock.lock();
         side = side_stream(stream_device(s));

@@ -230,18 +230,26 @@ __device__ __forceinline__ TileInfo tile_info(const Params& p, const int* g, int
     return ti;
 }
 
-__device__ __forceinline__ int range_sum(const int* c, int a, int b) {
-    int s = 0;
-    for (int i = a; i < b; ++i) s += c[i];
-    return s;
-}
-
-// Per tile: own sample count and number of work items (>= 1 so that every tile is stored).
-__device__ __forceinline__ void tile_totals(const Params& p, const int* g, int t, int& own, int& items) {
+// Per tile: own sample count and number of work items (>= 1 so that every tile is stored), and
+// the counts of its own bins (at most kKeyedBins) for the caller. Every count the tile needs (its
+// own bins, two bins of the left and of the upper neighbour, one of the upper-left) is requested
+// before any is used: one round trip instead of up to sixteen dependent ones, which made the two
+// scan launches latency-bound.
+__device__ __forceinline__ void tile_totals(const Params& p, const int* g, int t, int& own, int& items,
+                                            int (&c)[kKeyedBins]) {
     const TileInfo ti = tile_info(p, g, t);
-    own = range_sum(p.counts, ti.own0, ti.own1);
-    const int vis = own + range_sum(p.counts, ti.l0, ti.l1) + range_sum(p.counts, ti.u0, ti.u1) +
-                    range_sum(p.counts, ti.d0, ti.d1);
+    int e[5];
+#pragma unroll
+    for (int i = 0; i < kKeyedBins; ++i) c[i] = ti.own0 + i < ti.own1 ? p.counts[ti.own0 + i] : 0;
+    e[0] = ti.l0 < ti.l1 ? p.counts[ti.l0] : 0;
+    e[1] = ti.l0 + 1 < ti.l1 ? p.counts[ti.l0 + 1] : 0;
+    e[2] = ti.u0 < ti.u1 ? p.counts[ti.u0] : 0;
+    e[3] = ti.u0 + 1 < ti.u1 ? p.counts[ti.u0 + 1] : 0;
+    e[4] = ti.d0 < ti.d1 ? p.counts[ti.d0] : 0;
+    own = 0;
+#pragma unroll
+    for (int i = 0; i < kKeyedBins; ++i) own += c[i];
+    const int vis = own + e[0] + e[1] + e[2] + e[3] + e[4];
     items = vis > 0 ? (vis + kChunkRecords - 1) / kChunkRecords : 1;
 }
 
@@ -294,8 +302,8 @@ __global__ __launch_bounds__(256) void scan_reduce_kernel(Params p) {
     for (int i = 0; i < kTilesPerThread; ++i) {
         const int t = t0 + i;
         if (t >= p.n_tiles) break;
-        int own, items;
-        tile_totals(p, s_geo, t, own, items);
+        int own, items, c[kKeyedBins];
+        tile_totals(p, s_geo, t, own, items, c);
         own_sum += own;
         item_sum += items;
     }
@@ -321,13 +329,16 @@ __global__ __launch_bounds__(256) void scan_apply_kernel(Params p) {
     __shared__ int s_geo[kGeo * kMaxLevels];
     __shared__ int s[512];
     load_geo(p, s_geo);
-    int own[kTilesPerThread], items[kTilesPerThread];
+    static_assert(kTilesPerThread == 1, "one tile per scan thread");
+    int own[kTilesPerThread], items[kTilesPerThread], cnt[kKeyedBins];
     int own_sum = 0, item_sum = 0;
     const int t0 = blockIdx.x * kScanTiles + threadIdx.x * kTilesPerThread;
     for (int i = 0; i < kTilesPerThread; ++i) {
         const int t = t0 + i;
         own[i] = items[i] = 0;
-        if (t < p.n_tiles) tile_totals(p, s_geo, t, own[i], items[i]);
+#pragma unroll
+        for (int j = 0; j < kKeyedBins; ++j) cnt[j] = 0;
+        if (t < p.n_tiles) tile_totals(p, s_geo, t, own[i], items[i], cnt);
         own_sum += own[i];
         item_sum += items[i];
     }
@@ -340,10 +351,14 @@ __global__ __launch_bounds__(256) void scan_apply_kernel(Params p) {
         if (t >= p.n_tiles) break;
         int B;
         const int b0 = tile_bin0(p, s_geo, t, B);
-        for (int c = 0; c < B; ++c) {
-            p.offsets[b0 + c] = rec;
-            p.cursor[b0 + c] = rec;
-            rec += p.counts[b0 + c];
+        // the tile's own bins, counted above (B <= kKeyedBins)
+#pragma unroll
+        for (int c = 0; c < kKeyedBins; ++c) {
+            if (c < B) {
+                p.offsets[b0 + c] = rec;
+                p.cursor[b0 + c] = rec;
+                rec += cnt[c];
+            }
         }
         p.tile_chunks[t] = item;
         for (int c = 0; c < items[i] && item + c < p.max_items; ++c) p.items[item + c] = t;
@@ -682,7 +697,11 @@ constexpr int kGroups = 64 / kLPR;                // record streams per wave
 constexpr int kRunBatch = 2 * kLPR;               // records loaded together per stream (128 rows per wave)
 constexpr int kUnitRunMax = 12;                  // records per run up to which an item is folded by work units
 static_assert(kLPR == 2 || kLPR == 4 || kLPR == 8, "lanes per record");
+#ifndef MSDA_ABLATE_FOLD_ONE_QUEUE
 constexpr int kQueues = 8;                                 // fold work queues, one per XCD
+#else
+constexpr int kQueues = 1;
+#endif
 constexpr int kQueueStride = 64;                           // ints between queue counters (256 B)
 
 template <typename T, int VEC>
@@ -1357,6 +1376,12 @@ size_t align256(size_t x) { return (x + 255) / 256 * 256; }
 // resident. (Four or eight per CU, the extra ones exiting at once when they find the queues drained,
 // made the backward 0.5-1 % and 3-7 % slower.)
 int queue_grid(hipStream_t stream) {
+    const int cus = device_cu_count(stream);
+    return cus > 0 ? 2 * cus : -1;
+}
+}  // namespace
+
+int device_cu_count(hipStream_t stream) {
     constexpr int kDevs = 64;
     static std::atomic<int> cache[kDevs];
     // the device the work is enqueued on: the stream's (the current device for the null stream)
@@ -1374,11 +1399,9 @@ int queue_grid(hipStream_t stream) {
     }
     int cus = 0;
     if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return -1;
-    const int grid = 2 * cus;
-    if (dev >= 0 && dev < kDevs && grid > 0) cache[dev].store(grid, std::memory_order_relaxed);
-    return grid;
+    if (dev >= 0 && dev < kDevs && cus > 0) cache[dev].store(cus, std::memory_order_relaxed);
+    return cus;
 }
-}  // namespace
 
 // Ints of the workspace's zeroed head: the per-bin counts, the fold's queue counters and the scan's
 // count of finished workgroups, each counter on a 256-byte line of its own.

@@ -27,6 +27,8 @@ using rsrc_t = __amdgpu_buffer_rsrc_t;
 // backward reads them again.)
 typedef float stream_f4 __attribute__((ext_vector_type(4)));
 typedef float stream_f2 __attribute__((ext_vector_type(2)));
+typedef unsigned stream_u4 __attribute__((ext_vector_type(4)));
+#ifndef MSDA_ABLATE_PLAIN_STORES
 __device__ __forceinline__ void stream_store(float4* p, float4 x) {
     const stream_f4 v = {x.x, x.y, x.z, x.w};
     __builtin_nontemporal_store(v, reinterpret_cast<stream_f4*>(p));
@@ -36,11 +38,16 @@ __device__ __forceinline__ void stream_store(float2* p, float2 x) {
     __builtin_nontemporal_store(v, reinterpret_cast<stream_f2*>(p));
 }
 __device__ __forceinline__ void stream_store(float* p, float x) { __builtin_nontemporal_store(x, p); }
-typedef unsigned stream_u4 __attribute__((ext_vector_type(4)));
 __device__ __forceinline__ void stream_store(uint4* p, uint4 x) {
     const stream_u4 v = {x.x, x.y, x.z, x.w};
     __builtin_nontemporal_store(v, reinterpret_cast<stream_u4*>(p));
 }
+#else
+__device__ __forceinline__ void stream_store(float4* p, float4 x) { *p = x; }
+__device__ __forceinline__ void stream_store(float2* p, float2 x) { *p = x; }
+__device__ __forceinline__ void stream_store(float* p, float x) { *p = x; }
+__device__ __forceinline__ void stream_store(uint4* p, uint4 x) { *p = x; }
+#endif
 
 __device__ __forceinline__ rsrc_t make_rsrc(const void* p, uint32_t bytes) {
     return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, (int)bytes, kBufFlags);
@@ -172,11 +179,30 @@ struct Row<_Float16, VEC> {
 
 // ---------------------------------------------------------------- reductions over a lane group
 
+#ifndef MSDA_ABLATE_NO_DPP
 template <int CTRL>
 __device__ __forceinline__ float dpp(float v) {
     return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), CTRL,
                                                                  0xf, 0xf, false));
 }
+#else
+// the same lane permutations through ds_bpermute (the LDS crossbar) instead of DPP
+template <int CTRL>
+__device__ __forceinline__ float dpp(float v) {
+    const int lane = __lane_id();
+    int src = lane;
+    if constexpr (CTRL == 0xB1) src = lane ^ 1;                                  // quad_perm [1,0,3,2]
+    else if constexpr (CTRL == 0x4E) src = lane ^ 2;                             // quad_perm [2,3,0,1]
+    else if constexpr (CTRL == 0x141) src = (lane & ~7) | (7 - (lane & 7));      // row_half_mirror
+    else if constexpr (CTRL == 0x140) src = (lane & ~15) | (15 - (lane & 15));   // row_mirror
+    else if constexpr (CTRL == 0x104) src = (lane & 15) < 12 ? lane + 4 : lane;  // row_shl:4
+    else static_assert(CTRL == 0xB1, "lane permutation without a shuffle equivalent");
+    // every lane takes part in the shuffle (a lane must be active to be read from)
+    const float r = __shfl(v, src, 64);
+    if constexpr (CTRL == 0x104) return (lane & 15) < 12 ? r : 0.f;  // 0 past the row
+    return r;
+}
+#endif
 
 // Sum over the LPP consecutive lanes of a group; every lane of the group gets the total.
 // Steps 1-2 swap within quads (quad_perm), step 3 mirrors within 8 lanes (each lane meets the
@@ -214,12 +240,25 @@ struct Tile {
 __device__ __forceinline__ bool tile_of(const Params& p, int PPW, Tile& t) {
     const uint32_t G = gridDim.x;
     const uint32_t b = blockIdx.x;
+#ifndef MSDA_ABLATE_NO_XCD_REMAP
     const uint32_t w = (b & 7u) * (G >> 3) + (b >> 3);
+#else
+    const uint32_t w = b;
+    (void)G;
+#endif
     if (w >= (uint32_t)p.num_blocks) return false;
+#ifndef MSDA_ABLATE_HEAD_FASTEST
     const int slab = (int)(w / (uint32_t)p.chunks);
     const int chunk = (int)(w - (uint32_t)slab * (uint32_t)p.chunks);
     t.n = slab / p.M;
     t.m = slab - t.n * p.M;
+#else
+    // work items ordered (batch, query chunk, head): the heads of one chunk are consecutive
+    const int nc = (int)(w / (uint32_t)p.M);
+    t.m = (int)(w - (uint32_t)nc * (uint32_t)p.M);
+    t.n = nc / p.chunks;
+    const int chunk = nc - t.n * p.chunks;
+#endif
     t.q0 = chunk * p.q_per_block + (int)(threadIdx.x >> 6) * PPW;
     return true;
 }
@@ -304,6 +343,9 @@ __device__ __forceinline__ void load_levels(const Params& p, int* s_lvl) {
 // Channels per lane: the widest row piece (<= 16 bytes) that divides D.
 template <typename T>
 inline int pick_vec(int D) {
+#ifdef MSDA_ABLATE_VEC1
+    return 1;
+#endif
     constexpr int kMax = 16 / sizeof(T);
     for (int v = kMax; v > 1; v >>= 1)
         if (D % v == 0) return v;

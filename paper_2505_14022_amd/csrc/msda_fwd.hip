@@ -106,6 +106,173 @@ __global__ __launch_bounds__(kBlock) void fwd_kernel(Params p) {
     }
 }
 
+#ifdef MSDA_ABLATE_LDS_STAGE
+// Ablation: the forward with one coarse level (p.stage_level) of the workgroup's (batch, head)
+// slab copied into LDS first, its corner rows then read from LDS (a zero row past the level's
+// pixels stands for corners off the map). A workgroup runs p.stage_chunks consecutive query chunks
+// of its slab, so that each copied row is read several times.
+constexpr int kStageBytes = 32 * 1024;
+
+template <typename T, int VEC, int LPP>
+__global__ __launch_bounds__(kBlock) void fwd_staged_kernel(Params p) {
+    constexpr int PPW = 64 / LPP;
+    __shared__ int s_lvl[3 * kMaxLevels];
+    __shared__ int4 s_off[kWaves][kMaxItems];
+    __shared__ float4 s_w[kWaves][kMaxItems];
+    __shared__ __attribute__((aligned(16))) T s_stage[kStageBytes / sizeof(T)];
+    load_levels(p, s_lvl);
+    const uint32_t G = gridDim.x, b = blockIdx.x;
+    const uint32_t w = (b & 7u) * (G >> 3) + (b >> 3);
+    const int groups = (p.chunks + p.stage_chunks - 1) / p.stage_chunks;
+    if (w >= (uint32_t)(p.n_batch * p.M * groups)) return;
+    const int slab = (int)w / groups, group = (int)w - slab * groups;
+    const int n = slab / p.M, m = slab - n * p.M;
+    const int ls = p.stage_level;
+    const int Hs = s_lvl[ls], Ws = s_lvl[kMaxLevels + ls], sts = s_lvl[2 * kMaxLevels + ls];
+    const int npx = Hs * Ws;
+    const T* value = static_cast<const T*>(p.value);
+    // the level's rows of this slab, then one zero row, VEC channels (at most 16 bytes) per copy
+    for (int e = threadIdx.x * VEC; e < (npx + 1) * p.D; e += blockDim.x * VEC) {
+        const int px = e / p.D, ch = e - px * p.D;
+        float v[VEC];
+        if (px < npx) Row<T, VEC>::load_ptr(v, value + ((size_t)(n * p.S + sts + px) * p.M + m) * p.D + ch);
+        else
+#pragma unroll
+            for (int i = 0; i < VEC; ++i) v[i] = 0.f;
+        Row<T, VEC>::store(s_stage + e, v);
+    }
+    __syncthreads();
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    const int ps = lane / LPP, sub = lane % LPP;
+    const int K = p.K;
+    const int KC = K < kMaxItems / PPW ? K : kMaxItems / PPW;
+    const rsrc_t vr = make_rsrc(p.value, p.value_bytes);
+    T* out = static_cast<T*>(p.out);
+    for (int cg = 0; cg < p.stage_chunks; ++cg) {
+        const int chunk = group * p.stage_chunks + cg;
+        if (chunk >= p.chunks) break;
+        const int q0 = chunk * p.q_per_block + wave * PPW;
+        const int q_mine = q0 + ps;
+        for (int c0 = 0; c0 < p.D; c0 += LPP * VEC) {
+            const int chan = c0 + sub * VEC;
+            const bool active = chan < p.D;
+            const uint32_t chan_bytes = (uint32_t)chan << Row<T, VEC>::kShift;
+            float acc[VEC];
+#pragma unroll
+            for (int i = 0; i < VEC; ++i) acc[i] = 0.f;
+            for (int k0 = 0; k0 < K; k0 += KC) {
+                const int kn = K - k0 < KC ? K - k0 : KC;
+                wave_lds_sync();
+                for (int j = lane; j < PPW * kn; j += 64) {
+                    const int jq = j / kn, jk = j - jq * kn;
+                    SampleDesc sd;
+                    describe(p, s_lvl, n, m, q0 + jq, k0 + jk, true, sd);
+                    if ((k0 + jk) / p.P == ls) {
+                        // staged level: pixel within the level times D, or the zero row for corners
+                        // (and whole samples) off the map
+                        auto to_stage = [&](int o) {
+                            if (o == (int)kOOBElem) return npx * p.D;
+                            return ((o / p.D - m) / p.M - n * p.S - sts) * p.D;
+                        };
+                        sd.off = make_int4(to_stage(sd.off.x), to_stage(sd.off.y), to_stage(sd.off.z), to_stage(sd.off.w));
+                    }
+                    s_off[wave][j] = sd.off;
+                    s_w[wave][j] = sd.w;
+                }
+                wave_lds_sync();
+                if (active) {
+                    const int base = ps * kn;
+                    for (int kk = 0; kk < kn; ++kk) {
+                        const int4 off = s_off[wave][base + kk];
+                        const float4 wt = s_w[wave][base + kk];
+                        float v[4][VEC];
+                        const int o[4] = {off.x, off.y, off.z, off.w};
+                        // every query of the wave is at sample kk: the level is the same for all
+                        if ((k0 + kk) / p.P == ls) {
+#pragma unroll
+                            for (int c = 0; c < 4; ++c) Row<T, VEC>::load_ptr(v[c], s_stage + o[c] + chan);
+                        } else {
+#pragma unroll
+                            for (int c = 0; c < 4; ++c)
+                                Row<T, VEC>::load(v[c], vr, ((uint32_t)o[c] << Row<T, VEC>::kShift) + chan_bytes);
+                        }
+#pragma unroll
+                        for (int i = 0; i < VEC; ++i)
+                            acc[i] += wt.x * v[0][i] + wt.y * v[1][i] + wt.z * v[2][i] + wt.w * v[3][i];
+                    }
+                }
+            }
+            if (active && q_mine < p.Lq)
+                Row<T, VEC>::store_final(out + ((size_t)(n * p.Lq + q_mine) * p.M + m) * p.D + chan, acc);
+        }
+    }
+}
+
+template <typename T, int VEC, int LPP>
+struct FwdStagedK {
+    static auto fn() { return fwd_staged_kernel<T, VEC, LPP>; }
+};
+
+// The staged level (the largest that fits kStageBytes with its zero row) and the chunks per
+// workgroup (each staged row read about four times); false when no level fits.
+template <typename T>
+bool plan_stage(Params& p, int q_per_block) {
+    p.stage_level = -1;
+    int best = 0;
+    for (int l = 0; l < p.L; ++l) {
+        const int64_t px = (int64_t)p.H[l] * p.W[l];
+        if ((px + 1) * p.D * (int64_t)sizeof(T) <= kStageBytes && px > best) {
+            best = (int)px;
+            p.stage_level = l;
+        }
+    }
+    if (p.stage_level < 0) return false;
+    const int64_t reads_per_chunk = (int64_t)q_per_block * p.P * 4;  // corner rows of one chunk at that level
+    int64_t c = (4 * (int64_t)best + reads_per_chunk - 1) / reads_per_chunk;
+    p.stage_chunks = (int)(c < 1 ? 1 : c > 16 ? 16 : c);
+    return true;
+}
+
+template <typename T, int VEC>
+hipError_t launch_staged_vec(Params p, int lpp, hipStream_t stream) {
+    auto go = [&](auto kernel, int ppw) -> hipError_t {
+        p.q_per_block = kWaves * ppw;
+        p.chunks = (p.Lq + p.q_per_block - 1) / p.q_per_block;
+        if (!plan_stage<T>(p, p.q_per_block)) return hipErrorNotSupported;
+        const int groups = (p.chunks + p.stage_chunks - 1) / p.stage_chunks;
+        p.num_blocks = p.n_batch * p.M * groups;
+        if (p.num_blocks == 0) return hipSuccess;
+        const int grid = (p.num_blocks + 7) / 8 * 8;
+        hipLaunchKernelGGL(kernel, dim3(grid), dim3(kBlock), 0, stream, p);
+        return hipGetLastError();
+    };
+    switch (lpp) {
+        case 1: return go(FwdStagedK<T, VEC, 1>::fn(), 64);
+        case 2: return go(FwdStagedK<T, VEC, 2>::fn(), 32);
+        case 4: return go(FwdStagedK<T, VEC, 4>::fn(), 16);
+        case 8: return go(FwdStagedK<T, VEC, 8>::fn(), 8);
+        case 16: return go(FwdStagedK<T, VEC, 16>::fn(), 4);
+        case 32: return go(FwdStagedK<T, VEC, 32>::fn(), 2);
+        default: return go(FwdStagedK<T, VEC, 64>::fn(), 1);
+    }
+}
+
+// hipErrorNotSupported when no level fits: the caller launches the plain forward instead
+template <typename T>
+hipError_t launch_staged(const Params& p, hipStream_t stream) {
+    const int vec = pick_vec<T>(p.D);
+    const int lpp = pick_lpp(p.D, vec);
+    switch (vec) {
+        case 1: return launch_staged_vec<T, 1>(p, lpp, stream);
+        case 2: return launch_staged_vec<T, 2>(p, lpp, stream);
+        case 4: return launch_staged_vec<T, 4>(p, lpp, stream);
+        default:
+            if constexpr (sizeof(T) == 2) return launch_staged_vec<T, 8>(p, lpp, stream);
+            return hipErrorInvalidValue;
+    }
+}
+#endif  // MSDA_ABLATE_LDS_STAGE
+
 template <typename T, int VEC, int LPP>
 struct FwdK {
     static auto fn() { return fwd_kernel<T, VEC, LPP, false>; }
@@ -118,6 +285,12 @@ struct FwdFusedK {
 }  // namespace
 
 hipError_t launch_forward(const Params& p, msda_dtype_t dtype, hipStream_t stream) {
+#ifdef MSDA_ABLATE_LDS_STAGE
+    {
+        const hipError_t e = dtype == MSDA_F16 ? launch_staged<_Float16>(p, stream) : launch_staged<float>(p, stream);
+        if (e != hipErrorNotSupported) return e;
+    }
+#endif
     return dtype == MSDA_F16 ? launch_typed<FwdK, _Float16>(p, stream) : launch_typed<FwdK, float>(p, stream);
 }
 

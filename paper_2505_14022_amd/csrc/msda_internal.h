@@ -6,6 +6,18 @@
 
 #include "msda.h"
 
+// Ablation builds (never the product library): each MSDA_ABLATE_* macro, set on the compiler
+// command line by microbench/ablation.py, replaces one design choice with a complete, correct
+// alternative, so that the choice can be timed and counted against the product build.
+//   MSDA_ABLATE_NO_XCD_REMAP    workgroup b runs work item b (no slab-per-XCD renumbering)
+//   MSDA_ABLATE_HEAD_FASTEST    work items in (batch, query chunk, head) order instead of slab-major
+//   MSDA_ABLATE_VEC1            one channel per lane (D lanes per query) instead of 16-byte pieces
+//   MSDA_ABLATE_NO_DPP          lane-group sums and maxima by ds_bpermute shuffles instead of DPP
+//   MSDA_ABLATE_PLAIN_STORES    outputs written with ordinary stores instead of nontemporal ones
+//   MSDA_ABLATE_ONE_STREAM      the owner-computes backward on the caller's stream alone
+//   MSDA_ABLATE_FOLD_ONE_QUEUE  one work-queue counter for the fold instead of one per XCD
+//   MSDA_ABLATE_LDS_STAGE       the forward stages the largest level that fits 32 KB in LDS
+
 namespace msda {
 
 constexpr int kMaxLevels = MSDA_MAX_LEVELS;
@@ -50,6 +62,8 @@ struct Params {
     int chunks;            // ceil(Lq / q_per_block)
     int num_blocks;        // n_batch * M * chunks (the grid is padded to a multiple of 8)
     int H[kMaxLevels], W[kMaxLevels], start[kMaxLevels];
+    int stage_level;       // forward, MSDA_ABLATE_LDS_STAGE only: level staged in LDS (-1: none)
+    int stage_chunks;      // forward, MSDA_ABLATE_LDS_STAGE only: query chunks per workgroup
 
     // ---- binned grad_value (owner-computes); filled by plan_binned() ----
     int tile_lh[kMaxLevels];    // log2 of the tile height at level l
@@ -108,6 +122,10 @@ hipError_t launch_binned_reset(const Params& p, hipStream_t stream);
 // grad_value by binning samples per destination tile and accumulating each tile once.
 hipError_t launch_backward_value_binned(const Params& p, msda_dtype_t dtype, hipStream_t stream);
 hipError_t launch_zero(float* ptr, int64_t n, hipStream_t stream);
+
+// Compute units of the device `stream` belongs to (the current device for the null stream),
+// cached per device; -1 on error.
+int device_cu_count(hipStream_t stream);
 
 // Device address of the static scratch array (kStaticScratchBytes) on `device`, looked up on the
 // first call for that device; no allocation.

@@ -13,7 +13,8 @@ from typing import Optional, Sequence, Tuple
 import numpy as np
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_PKG, "_lib", "libmsda.so")
+# MSDA_LIBRARY names another build of the same library (the ablation builds of microbench/ablation.py)
+LIB_PATH = os.environ.get("MSDA_LIBRARY") or os.path.join(_PKG, "_lib", "libmsda.so")
 
 MSDA_SUCCESS = 0
 MSDA_ERROR_INVALID_VALUE = 1
