@@ -32,11 +32,16 @@ sys.path.insert(0, ROOT)
 
 # variant -> (macro, what it replaces, workloads it is measured at)
 VARIANTS = {
-    "no_xcd_remap": ("MSDA_ABLATE_NO_XCD_REMAP", "workgroups renumbered so that one (batch, head) slab runs on one XCD",
+    "no_xcd_remap": ("MSDA_ABLATE_NO_XCD_REMAP", "work arranged over the XCDs: query eighths where the queries are at "
+                     "least half the value pixels, slab ranges elsewhere (variant: workgroup b runs work item b)",
                      ["detr_encoder", "bev_tsa_f16", "swin5_f16"]),
-    "head_fastest": ("MSDA_ABLATE_HEAD_FASTEST", "work items in (batch, head, query chunk) order, each XCD a contiguous "
-                     "eighth (variant: (batch, query chunk, head) order, the heads of a chunk consecutive)",
-                     ["detr_encoder", "bev_tsa_f16"]),
+    "head_fastest": ("MSDA_ABLATE_HEAD_FASTEST", "work items in (batch, head, query chunk) order, query eighths or "
+                     "slab ranges per XCD (variant: slab ranges in (batch, query chunk, head) order, the heads of a "
+                     "chunk consecutive)", ["detr_encoder", "bev_tsa_f16"]),
+    "slab_ranges": ("MSDA_ABLATE_SLAB_RANGES", "query eighths per XCD where the queries are at least half the value "
+                    "pixels (variant: slab ranges on every shape)", ["detr_encoder", "bev_tsa_f16", "swin5_f16"]),
+    "query_eighths": ("MSDA_ABLATE_QUERY_EIGHTHS", "slab ranges per XCD where the queries are fewer than half the value "
+                      "pixels (variant: query eighths on every shape)", ["bev_sca", "detr_decoder"]),
     "vec1": ("MSDA_ABLATE_VEC1", "16-byte row pieces per lane (8 lanes x float4 per 128-byte row at D = 32)",
              ["detr_encoder"]),
     "no_dpp": ("MSDA_ABLATE_NO_DPP", "DPP lane permutations in the channel reductions (transposed corner sums)",

@@ -9,8 +9,11 @@
 // Ablation builds (never the product library): each MSDA_ABLATE_* macro, set on the compiler
 // command line by microbench/ablation.py, replaces one design choice with a complete, correct
 // alternative, so that the choice can be timed and counted against the product build.
-//   MSDA_ABLATE_NO_XCD_REMAP    workgroup b runs work item b (no slab-per-XCD renumbering)
+//   MSDA_ABLATE_NO_XCD_REMAP    workgroup b runs work item b on every shape (no XCD-aware arrangement)
 //   MSDA_ABLATE_HEAD_FASTEST    work items in (batch, query chunk, head) order instead of slab-major
+//                               (slab ranges on every shape)
+//   MSDA_ABLATE_SLAB_RANGES     slab ranges per XCD on every shape (no query eighths)
+//   MSDA_ABLATE_QUERY_EIGHTHS   query eighths per XCD on every shape
 //   MSDA_ABLATE_VEC1            one channel per lane (D lanes per query) instead of 16-byte pieces
 //   MSDA_ABLATE_NO_DPP          lane-group sums and maxima by ds_bpermute shuffles instead of DPP
 //   MSDA_ABLATE_PLAIN_STORES    outputs written with ordinary stores instead of nontemporal ones
@@ -60,7 +63,8 @@ struct Params {
     int n_batch, S, M, D, Lq, L, P, K;  // K = L*P samples per (query, head)
     int q_per_block;       // queries of one (n, m) handled by one workgroup
     int chunks;            // ceil(Lq / q_per_block)
-    int num_blocks;        // n_batch * M * chunks (the grid is padded to a multiple of 8)
+    int xcd_split;         // forward / bwd_kernel work arrangement (tile_of): 1 query eighths, 0 slab ranges
+    int num_blocks;        // n_batch * M * chunks (the launch grid may be larger: see tile_of)
     int H[kMaxLevels], W[kMaxLevels], start[kMaxLevels];
     int stage_level;       // forward, MSDA_ABLATE_LDS_STAGE only: level staged in LDS (-1: none)
     int stage_chunks;      // forward, MSDA_ABLATE_LDS_STAGE only: query chunks per workgroup

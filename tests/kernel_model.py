@@ -7,7 +7,10 @@ code launches it and as each lane forms its addresses:
   * the host's batch split (largest batch count per launch that keeps element offsets below
     2^29) and the launch geometry (channels per lane, lanes per query, queries per wave, grid
     padded to a multiple of 8);
-  * the workgroup -> (batch, head, query chunk) renumbering that keeps a slab on one XCD;
+  * the workgroup -> (batch, head, query chunk) arrangement over the eight XCDs: query eighths
+    (XCD x takes the x-th eighth of every slab's query chunks) when there are at least half as many
+    queries as value pixels, else slab ranges (XCD x takes a contiguous eighth of the slab-major
+    work items);
   * the per-sample description: fp32 image coordinates, the open range test, floor, the int32
     element offset of each corner row, and the out-of-range sentinel (2^29 elements) for corners
     off the map, samples off the map and queries past Lq;
@@ -81,6 +84,7 @@ class Launch:
     chunks: int
     num_blocks: int
     grid: int
+    split: bool
 
 
 class AddressError(AssertionError):
@@ -100,8 +104,10 @@ def launches(N, S, M, D, Lq, L, P, es):
         qpb = waves * ppw
         chunks = (Lq + qpb - 1) // qpb
         num_blocks = cnt * M * chunks
-        grid = (num_blocks + 7) // 8 * 8
-        out.append(Launch(n0, cnt, vec, lpp, ppw, waves, qpb, chunks, num_blocks, grid))
+        split_grid = 8 * cnt * M * ((chunks + 7) // 8)
+        split = 2 * Lq >= S and split_grid <= MAX_INDEX
+        grid = split_grid if split else (num_blocks + 7) // 8 * 8
+        out.append(Launch(n0, cnt, vec, lpp, ppw, waves, qpb, chunks, num_blocks, grid, split))
     return out
 
 
@@ -111,13 +117,27 @@ def _check(cond, msg):
 
 
 def wave_queries(ln: Launch, M: int):
-    """(n, m, q) of every query slot of every wave of the launch, in the kernel's mapping
-    (workgroup b runs w = (b % 8) * (G / 8) + b / 8; slab-major work items)."""
+    """(n, m, q) of every query slot of every wave of the launch, in the kernel's mapping: with
+    x = b % 8 and i = b / 8, workgroup b runs chunk x*chunks/8 + i % per of slab i / per (query
+    eighths, per = ceil(chunks / 8)) or work item w = x * (G / 8) + i in slab-major order (slab
+    ranges). Every (slab, chunk) must be run exactly once."""
     b = np.arange(ln.grid, dtype=np.int64)
-    w = (b & 7) * (ln.grid >> 3) + (b >> 3)
-    _check(np.unique(w).size == ln.grid, "workgroup renumbering is not a permutation")
-    w = w[w < ln.num_blocks]
-    slab, chunk = w // ln.chunks, w % ln.chunks
+    x, i = b & 7, b >> 3
+    if ln.split:
+        per = (ln.chunks + 7) // 8
+        slab = i // per
+        chunk = ((x * ln.chunks) >> 3) + i % per
+        keep = (slab < ln.cnt * M) & (chunk < (((x + 1) * ln.chunks) >> 3))
+        slab, chunk = slab[keep], chunk[keep]
+    else:
+        w = x * (ln.grid >> 3) + i
+        _check(np.unique(w).size == ln.grid, "workgroup renumbering is not a permutation")
+        w = w[w < ln.num_blocks]
+        slab, chunk = w // ln.chunks, w % ln.chunks
+    item = slab * ln.chunks + chunk
+    _check((chunk >= 0) & (chunk < ln.chunks), "work item chunk out of range")
+    _check((np.unique(item).size == item.size) & (item.size == ln.num_blocks),
+           "work items not covered exactly once")
     n, m = slab // M, slab % M
     wave = np.arange(ln.waves, dtype=np.int64)
     ps = np.arange(ln.ppw, dtype=np.int64)

@@ -73,3 +73,18 @@ def test_model_catches_a_planted_offset_error(step):
     with pytest.raises(AddressError):
         model_atomic_backward(inp.value, inp.shapes, inp.starts, inp.loc, inp.attn, inp.grad_out,
                               plant_col_step=step)
+
+
+def test_both_xcd_arrangements_are_modelled():
+    # query eighths where queries are at least half the value pixels, slab ranges elsewhere; the
+    # cases above exercise both
+    from kernel_model import launches
+
+    def split(N, M, D, shapes, P, Lq, dt):
+        S = sum(h * w for h, w in shapes)
+        return {ln.split for ln in launches(N, S, M, D, Lq, len(shapes), P, 2 if dt == "f16" else 4)}
+
+    assert {True, False} <= set().union(*(split(*c) for c in SMALL))
+    enc, dec = workloads.BY_NAME["detr_encoder"], workloads.BY_NAME["detr_decoder"]
+    assert split(enc.N, enc.M, enc.D, enc.shapes, enc.P, enc.Lq, enc.dtype) == {True}
+    assert split(dec.N, dec.M, dec.D, dec.shapes, dec.P, dec.Lq, dec.dtype) == {False}
