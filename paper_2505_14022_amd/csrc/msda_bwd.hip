@@ -22,6 +22,10 @@ namespace {
 constexpr int kBwdU = MSDA_BWD_UNROLL;
 // grad_out floats of one wave's queries staged in LDS by the atomic variant (PPW * D at most)
 constexpr int kAtomicRowFloats = 512;
+#ifndef MSDA_KSPLIT_MAX
+#define MSDA_KSPLIT_MAX 8
+#endif
+constexpr int kMaxKSplit = MSDA_KSPLIT_MAX;  // most parts a query's samples are split into
 
 
 // Sums each of the four corner dot products over the query's LPP lanes and stores the four totals
@@ -96,8 +100,11 @@ __global__ __launch_bounds__(kBlock) void bwd_kernel(Params p) {
         }
     }
 
-    for (int k0 = 0; k0 < K; k0 += KC) {
-        const int kn = K - k0 < KC ? K - k0 : KC;
+    // the samples [kb, ke) of this workgroup's part
+    const int kper = (K + p.k_split - 1) / p.k_split;
+    const int kb = t.part * kper, ke = kb + kper < K ? kb + kper : K;
+    for (int k0 = kb; k0 < ke; k0 += KC) {
+        const int kn = ke - k0 < KC ? ke - k0 : KC;
         wave_lds_sync();
         for (int j = lane; j < PPW * kn; j += 64) {
             const int jq = j / kn, jk = j - jq * kn;
@@ -328,7 +335,11 @@ __global__ __launch_bounds__(256) void zero_kernel(float4* p, int64_t n4, float*
 
 }  // namespace
 
-hipError_t launch_backward_grads(const Params& p, msda_dtype_t dtype, bool atomic_grad_value, hipStream_t stream) {
+hipError_t launch_backward_grads(const Params& p0, msda_dtype_t dtype, bool atomic_grad_value, hipStream_t stream) {
+    // every output of a sample depends on that sample alone, so small grids may split a query's
+    // samples over several workgroups; the fused chain rule needs all of them in one wave
+    Params p = p0;
+    p.k_split_max = p.prologue_grads ? 1 : kMaxKSplit;
     if (atomic_grad_value)
         return dtype == MSDA_F16 ? launch_typed<BwdAtomicK, _Float16>(p, stream)
                                  : launch_typed<BwdAtomicK, float>(p, stream);

@@ -233,6 +233,7 @@ __device__ __forceinline__ float group_sum(float v) {
 
 struct Tile {
     int n, m, q0;  // slab (n, m) and the first query of this wave
+    int part;      // which of the p.k_split parts of the queries' samples this workgroup takes
 };
 
 // Workgroup -> (slab, query chunk). Workgroup b runs on XCD b % 8 (the dispatcher deals workgroups
@@ -273,6 +274,12 @@ __device__ __forceinline__ bool tile_of(const Params& p, int PPW, Tile& t) {
     }
     t.n = slab / p.M;
     t.m = slab - t.n * p.M;
+    t.part = 0;
+    if (p.k_split > 1) {
+        // the parts of one query chunk are consecutive work items
+        t.part = chunk % p.k_split;
+        chunk /= p.k_split;
+    }
     t.q0 = chunk * p.q_per_block + (int)(threadIdx.x >> 6) * PPW;
     return true;
 }
@@ -398,13 +405,29 @@ inline int pick_lpp(int D, int vec) {
 // the other waves of its workgroup, and at the DETR-decoder shape (160 four-wave workgroups)
 // one-wave workgroups spread the grad_value atomics over all CUs.
 constexpr int kSmallGrid = 1024;
+#ifndef MSDA_KSPLIT_WAVES
+#define MSDA_KSPLIT_WAVES 4096
+#endif
+constexpr int64_t kSplitWaves = MSDA_KSPLIT_WAVES;  // waves a sample split may grow the grid to
+#ifndef MSDA_KSPLIT_MIN
+#define MSDA_KSPLIT_MIN 4
+#endif
+constexpr int kSplitMinSamples = MSDA_KSPLIT_MIN;
 template <template <typename, int, int> class KernelT, typename T, int VEC>
 hipError_t launch_lpp(Params p, int lpp, hipStream_t stream) {
     auto go = [&](auto kernel, int ppw) -> hipError_t {
         const int64_t chunks4 = (p.Lq + kWaves * ppw - 1) / (kWaves * ppw);
         const int waves = (int64_t)p.n_batch * p.M * chunks4 < kSmallGrid ? 1 : kWaves;
         p.q_per_block = waves * ppw;
-        p.chunks = (p.Lq + p.q_per_block - 1) / p.q_per_block;
+        const int qchunks = (p.Lq + p.q_per_block - 1) / p.q_per_block;
+        // a grid too small to fill the chip splits each query's samples over up to k_split_max
+        // work items, as long as a part keeps kSplitMinSamples samples
+        int ks = 1;
+        while (2 * ks <= p.k_split_max && 2 * ks * kSplitMinSamples <= p.K &&
+               (int64_t)p.n_batch * p.M * qchunks * waves * 2 * ks <= kSplitWaves)
+            ks *= 2;
+        p.k_split = ks;
+        p.chunks = qchunks * ks;
         p.num_blocks = p.n_batch * p.M * p.chunks;
         if (p.num_blocks == 0) return hipSuccess;
         const int64_t split_grid = 8 * (int64_t)p.n_batch * p.M * ((p.chunks + 7) / 8);

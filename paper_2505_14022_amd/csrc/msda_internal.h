@@ -62,7 +62,9 @@ struct Params {
     uint32_t gv_bytes;     // size of the grad_value buffer resource
     int n_batch, S, M, D, Lq, L, P, K;  // K = L*P samples per (query, head)
     int q_per_block;       // queries of one (n, m) handled by one workgroup
-    int chunks;            // ceil(Lq / q_per_block)
+    int chunks;            // work items per slab: ceil(Lq / q_per_block) * k_split
+    int k_split;           // bwd_kernel: a query chunk's samples are split over k_split work items
+    int k_split_max;       // set by the launcher: the largest k_split it accepts (0 or 1: none)
     int xcd_split;         // forward / bwd_kernel work arrangement (tile_of): 1 query eighths, 0 slab ranges
     int num_blocks;        // n_batch * M * chunks (the launch grid may be larger: see tile_of)
     int H[kMaxLevels], W[kMaxLevels], start[kMaxLevels];

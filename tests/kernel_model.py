@@ -11,6 +11,8 @@ code launches it and as each lane forms its addresses:
     (XCD x takes the x-th eighth of every slab's query chunks) when there are at least half as many
     queries as value pixels, else slab ranges (XCD x takes a contiguous eighth of the slab-major
     work items);
+  * the sample split of small grids: a query chunk's K samples divided over up to 8 consecutive
+    work items (at least 4 samples each, at most 4096 waves in all);
   * the per-sample description: fp32 image coordinates, the open range test, floor, the int32
     element offset of each corner row, and the out-of-range sentinel (2^29 elements) for corners
     off the map, samples off the map and queries past Lq;
@@ -34,6 +36,9 @@ MAX_INDEX = (1 << 31) - 1
 WAVES_PER_BLOCK = 4
 SMALL_GRID = 1024        # below this many four-wave workgroups, workgroups of one wave are launched
 ATOMIC_ROW_FLOATS = 512  # grad_out floats of one wave staged for the row-coalesced atomics
+K_SPLIT_MAX = 8          # most parts the backward splits a query chunk's samples into ...
+K_SPLIT_MIN_SAMPLES = 4  # ... keeping at least this many samples per part ...
+K_SPLIT_WAVES = 4096     # ... while the grid stays within this many waves
 U32 = 1 << 32
 
 
@@ -85,6 +90,7 @@ class Launch:
     num_blocks: int
     grid: int
     split: bool
+    k_split: int
 
 
 class AddressError(AssertionError):
@@ -102,12 +108,17 @@ def launches(N, S, M, D, Lq, L, P, es):
         chunks4 = (Lq + WAVES_PER_BLOCK * ppw - 1) // (WAVES_PER_BLOCK * ppw)
         waves = 1 if cnt * M * chunks4 < SMALL_GRID else WAVES_PER_BLOCK
         qpb = waves * ppw
-        chunks = (Lq + qpb - 1) // qpb
+        qchunks = (Lq + qpb - 1) // qpb
+        ks = 1
+        while (2 * ks <= K_SPLIT_MAX and 2 * ks * K_SPLIT_MIN_SAMPLES <= L * P and
+               cnt * M * qchunks * waves * 2 * ks <= K_SPLIT_WAVES):
+            ks *= 2
+        chunks = qchunks * ks
         num_blocks = cnt * M * chunks
         split_grid = 8 * cnt * M * ((chunks + 7) // 8)
         split = 2 * Lq >= S and split_grid <= MAX_INDEX
         grid = split_grid if split else (num_blocks + 7) // 8 * 8
-        out.append(Launch(n0, cnt, vec, lpp, ppw, waves, qpb, chunks, num_blocks, grid, split))
+        out.append(Launch(n0, cnt, vec, lpp, ppw, waves, qpb, chunks, num_blocks, grid, split, ks))
     return out
 
 
@@ -117,10 +128,11 @@ def _check(cond, msg):
 
 
 def wave_queries(ln: Launch, M: int):
-    """(n, m, q) of every query slot of every wave of the launch, in the kernel's mapping: with
-    x = b % 8 and i = b / 8, workgroup b runs chunk x*chunks/8 + i % per of slab i / per (query
-    eighths, per = ceil(chunks / 8)) or work item w = x * (G / 8) + i in slab-major order (slab
-    ranges). Every (slab, chunk) must be run exactly once."""
+    """(n, m, q, part) of every query slot of every wave of the launch, in the kernel's mapping:
+    with x = b % 8 and i = b / 8, workgroup b runs chunk x*chunks/8 + i % per of slab i / per
+    (query eighths, per = ceil(chunks / 8)) or work item w = x * (G / 8) + i in slab-major order
+    (slab ranges). Every (slab, chunk) must be run exactly once; a work item is query chunk
+    chunk / k_split, sample part chunk % k_split."""
     b = np.arange(ln.grid, dtype=np.int64)
     x, i = b & 7, b >> 3
     if ln.split:
@@ -139,12 +151,13 @@ def wave_queries(ln: Launch, M: int):
     _check((np.unique(item).size == item.size) & (item.size == ln.num_blocks),
            "work items not covered exactly once")
     n, m = slab // M, slab % M
+    part, qchunk = chunk % ln.k_split, chunk // ln.k_split
     wave = np.arange(ln.waves, dtype=np.int64)
     ps = np.arange(ln.ppw, dtype=np.int64)
-    q = (chunk[:, None, None] * ln.q_per_block + wave[None, :, None] * ln.ppw + ps[None, None, :])
+    q = (qchunk[:, None, None] * ln.q_per_block + wave[None, :, None] * ln.ppw + ps[None, None, :])
     shp = q.shape
-    return (np.broadcast_to(n[:, None, None], shp).ravel(), np.broadcast_to(m[:, None, None], shp).ravel(),
-            q.ravel())
+    bc = lambda a: np.broadcast_to(a[:, None, None], shp).ravel()
+    return bc(n), bc(m), q.ravel(), bc(part)
 
 
 def coalesced_atomics(D: int, vec: int, lpp: int) -> bool:
@@ -220,26 +233,34 @@ def model_atomic_backward(value, shapes, starts, loc, attn, grad_out, plant_col_
         _check(elems < MAX_LAUNCH_ELEMS, "launch exceeds the element limit")
         _check(ln.cnt * Lq * M * K * 2 <= MAX_INDEX and ln.cnt * Lq * M * D <= MAX_INDEX,
                "per-launch sample index range exceeds int32")
-        n, m, q = wave_queries(ln, M)
-        # every real (n, m, q) of the launch is served exactly once; the rest are tail slots
+        n, m, q, part = wave_queries(ln, M)
+        # every real (n, m, q, part) of the launch is served exactly once; the rest are tail slots
         real = q < Lq
-        key = (n[real] * M + m[real]) * Lq + q[real]
-        _check(np.unique(key).size == key.size == ln.cnt * M * Lq, "queries not covered exactly once")
-        stats["sample_slots"] += int(real.sum()) * K
-        stats["tail_slots"] += int((~real).sum()) * K
+        key = ((n[real] * M + m[real]) * Lq + q[real]) * ln.k_split + part[real]
+        _check(np.unique(key).size == key.size == ln.cnt * M * Lq * ln.k_split, "queries not covered exactly once")
+        # the part's samples [kb, ke), as the kernel forms them
+        kper = (K + ln.k_split - 1) // ln.k_split
+        kb = part * kper
+        ke = np.minimum(kb + kper, K)
         # grad_out row read by each query slot (tail slots read query 0's row)
         gout_row = ((n * Lq + np.where(real, q, 0)) * M + m) * D
         _check((gout_row >= 0) & (gout_row + D <= ln.cnt * Lq * M * D), "grad_out row out of range")
+        covered = np.zeros(K, dtype=np.int64)
         for k in range(K):
             l = k // P
-            qq = np.where(real, q, 0)
-            smp = ((n * Lq + qq) * M + m) * K + k
-            _check(smp[real] < ln.cnt * Lq * M * K, "sample index out of range")
+            mine = (k >= kb) & (k < ke)  # the slots whose part holds sample k
+            covered[k] = int(np.count_nonzero(mine & real))
+            stats["sample_slots"] += int(np.count_nonzero(mine & real))
+            stats["tail_slots"] += int(np.count_nonzero(mine & ~real))
+            kn, km, kq, kreal, kgrow = n[mine], m[mine], q[mine], real[mine], gout_row[mine]
+            qq = np.where(kreal, kq, 0)
+            smp = ((kn * Lq + qq) * M + km) * K + k
+            _check(smp[kreal] < ln.cnt * Lq * M * K, "sample index out of range")
             xy = loc[ln.n0:ln.n0 + ln.cnt].reshape(-1, 2)[smp]
             a = attn[ln.n0:ln.n0 + ln.cnt].reshape(-1)[smp].astype(np.float32)
-            x = np.where(real, xy[:, 0], np.float32(-2.0)).astype(np.float32)
-            y = np.where(real, xy[:, 1], np.float32(-2.0)).astype(np.float32)
-            a = np.where(real, a, np.float32(0.0))
+            x = np.where(kreal, xy[:, 0], np.float32(-2.0)).astype(np.float32)
+            y = np.where(kreal, xy[:, 1], np.float32(-2.0)).astype(np.float32)
+            a = np.where(kreal, a, np.float32(0.0))
             w_im = fmaf32(x, W[l], -0.5)
             h_im = fmaf32(y, H[l], -0.5)
             ok = (h_im > -1) & (w_im > -1) & (h_im < H[l]) & (w_im < W[l])
@@ -250,7 +271,7 @@ def model_atomic_backward(value, shapes, starts, loc, attn, grad_out, plant_col_
             lw = np.where(ok, w_im - w0f, 0).astype(np.float32)
             hh, hw = np.float32(1) - lh, np.float32(1) - lw
             a = np.where(ok, a, np.float32(0))
-            base = ((n * S + st[l] + h0 * W[l] + w0) * M + m) * D
+            base = ((kn * S + st[l] + h0 * W[l] + w0) * M + km) * D
             _check(np.abs(base[ok]) <= MAX_INDEX, "corner base offset overflows int32")
             top, bot, lef, rig = h0 >= 0, h0 + 1 < H[l], w0 >= 0, w0 + 1 < W[l]
             corners = [(top & lef, base, a * (hh * hw)),
@@ -273,15 +294,17 @@ def model_atomic_backward(value, shapes, starts, loc, attn, grad_out, plant_col_
                     _check((byte + 4 <= gv_bytes) == valid, "an atomic lands iff its corner is on the map")
                 # a landed corner is the row of pixel (h0+dh, w0+dw) of this (batch, head)
                 hc, wc = h0 + dh_dw[0], w0 + dh_dw[1]
-                want = ((n * S + st[l] + hc * W[l] + wc) * M + m) * D
+                want = ((kn * S + st[l] + hc * W[l] + wc) * M + km) * D
                 _check(off[valid] == want[valid], "landed corner is not the sampled pixel's row")
                 _check(off[valid] % D == 0, "corner offset is not a row start")
                 stats["corner_atomics_landed"] += int(valid.sum()) * D
                 stats["corner_atomics_dropped"] += int((~valid).sum()) * D
                 # accumulate: grad_value[row] += w * g[query row]
                 rows = (off[valid] // D) + ln.n0 * S * M
-                cols = gout_row[valid] // D + ln.n0 * Lq * M
+                cols = kgrow[valid] // D + ln.n0 * Lq * M
                 if rows.size:
                     A = sp.coo_matrix((wgt[valid].astype(np.float64), (rows, cols)), shape=(N * S * M, N * Lq * M))
                     gv += A.tocsr() @ g
+        # each sample of each query is taken by exactly one part
+        _check(np.all(covered == ln.cnt * M * Lq), "a sample of some query is in no part or in two")
     return gv.reshape(N, S, M, D), stats

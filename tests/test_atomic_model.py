@@ -88,3 +88,12 @@ def test_both_xcd_arrangements_are_modelled():
     enc, dec = workloads.BY_NAME["detr_encoder"], workloads.BY_NAME["detr_decoder"]
     assert split(enc.N, enc.M, enc.D, enc.shapes, enc.P, enc.Lq, enc.dtype) == {True}
     assert split(dec.N, dec.M, dec.D, dec.shapes, dec.P, dec.Lq, dec.dtype) == {False}
+
+
+def test_small_grids_split_samples():
+    # the DETR-decoder grid (608 one-wave workgroups) splits each query's 16 samples in 4 parts;
+    # the encoder's grid is large enough as it is
+    from kernel_model import launches
+    dec, enc = workloads.BY_NAME["detr_decoder"], workloads.BY_NAME["detr_encoder"]
+    assert {ln.k_split for ln in launches(dec.N, dec.S, dec.M, dec.D, dec.Lq, dec.L, dec.P, 4)} == {4}
+    assert {ln.k_split for ln in launches(enc.N, enc.S, enc.M, enc.D, enc.Lq, enc.L, enc.P, 4)} == {1}
