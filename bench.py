@@ -153,22 +153,30 @@ def cpu_baseline(inp, budget_s: float = 10.0, fused: bool = False):
     import oracle
 
     steps, th = 0, 0
+    t_fwd = t_bwd = 0.0
     t0 = time.perf_counter()
     while True:
+        ta = time.perf_counter()
         if fused:
             loc, attn = oracle.prologue(inp.ref, inp.offsets, inp.logits, inp.shapes)
             _, th = oracle.forward(inp.value, inp.shapes, inp.starts, loc, attn, return_threads=True)
+            tb = time.perf_counter()
             oracle.backward_fused(inp.value, inp.shapes, inp.starts, inp.ref, inp.offsets, inp.logits,
                                   inp.grad_out)
         else:
             _, th = oracle.forward(inp.value, inp.shapes, inp.starts, inp.loc, inp.attn, return_threads=True)
+            tb = time.perf_counter()
             oracle.backward(inp.value, inp.shapes, inp.starts, inp.loc, inp.attn, inp.grad_out)
+        tc = time.perf_counter()
+        t_fwd += tb - ta
+        t_bwd += tc - tb
         steps += 1
         dt = time.perf_counter() - t0
         if dt >= budget_s or (steps >= 1 and dt * (steps + 1) / steps > 3 * budget_s):
             break
     return {"value": round(inp.w.samples * steps / dt / 1e9, 6), "unit": "Gsamples/s", "cores": int(th),
-            "kind": "oracle", "seconds": round(dt, 3),
+            "kind": "oracle", "seconds": round(dt, 3), "fwd_ms": round(1e3 * t_fwd / steps, 3),
+            "bwd_ms": round(1e3 * t_bwd / steps, 3),
             "sample": f"{steps} full {'fused ' if fused else ''}forward+backward steps of the {inp.w.name} "
                       f"workload ({inp.w.samples} samples each), fp64 oracle, OpenMP threads={th}"}
 
