@@ -229,6 +229,27 @@ __device__ __forceinline__ float group_sum(float v) {
     return v;
 }
 
+// Softmax statistics over aligned groups of G lanes for a runtime G (a power of two, at most 64):
+// the steps of group_max / group_sum up to G, so the trees are theirs; every lane of the wave must
+// be active. Returns (max, 1 / sum of exp(z - max)) of the lane's group.
+__device__ __forceinline__ float2 group_softmax_stats(float z, int G) {
+    float mx = z;
+    if (G >= 2) mx = fmaxf(mx, dpp<0xB1>(mx));
+    if (G >= 4) mx = fmaxf(mx, dpp<0x4E>(mx));
+    if (G >= 8) mx = fmaxf(mx, dpp<0x141>(mx));
+    if (G >= 16) mx = fmaxf(mx, dpp<0x140>(mx));
+    if (G >= 32) mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+    if (G >= 64) mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+    float sum = expf(z - mx);
+    if (G >= 2) sum += dpp<0xB1>(sum);
+    if (G >= 4) sum += dpp<0x4E>(sum);
+    if (G >= 8) sum += dpp<0x141>(sum);
+    if (G >= 16) sum += dpp<0x140>(sum);
+    if (G >= 32) sum += __shfl_xor(sum, 16, 64);
+    if (G >= 64) sum += __shfl_xor(sum, 32, 64);
+    return make_float2(mx, 1.f / sum);
+}
+
 // ---------------------------------------------------------------- work decomposition
 
 struct Tile {

@@ -41,16 +41,22 @@ __global__ __launch_bounds__(kBlock) void fwd_kernel(Params p) {
     const int KC = K < kMaxItems / PPW ? K : kMaxItems / PPW;
     const rsrc_t vr = make_rsrc(p.value, p.value_bytes);
     T* out = static_cast<T*>(p.out);
+    // FUSED with a query's K samples one aligned group of lanes in one pass of phase 1 (K a power of
+    // two, all K in one chunk): the softmax is formed there, from the one read of each logit;
+    // otherwise its statistics are gathered first, each query by its own lanes
+    const bool softmax_in_pass = FUSED && (K & (K - 1)) == 0 && K <= KC && K <= 64;
     if constexpr (FUSED) {
         const int q = q_mine < p.Lq ? q_mine : p.Lq - 1;
-        const float* z = p.logits + ((size_t)(t.n * p.Lq + q) * p.M + t.m) * K;
-        float mx = -INFINITY;
-        for (int k = sub; k < K; k += LPP) mx = fmaxf(mx, z[k]);
-        mx = group_max<LPP>(mx);
-        float sum = 0.f;
-        for (int k = sub; k < K; k += LPP) sum += expf(z[k] - mx);
-        sum = group_sum<LPP>(sum);
-        if (sub == 0) s_stat[wave][ps] = make_float2(mx, 1.f / sum);
+        if (!softmax_in_pass) {
+            const float* z = p.logits + ((size_t)(t.n * p.Lq + q) * p.M + t.m) * K;
+            float mx = -INFINITY;
+            for (int k = sub; k < K; k += LPP) mx = fmaxf(mx, z[k]);
+            mx = group_max<LPP>(mx);
+            float sum = 0.f;
+            for (int k = sub; k < K; k += LPP) sum += expf(z[k] - mx);
+            sum = group_sum<LPP>(sum);
+            if (sub == 0) s_stat[wave][ps] = make_float2(mx, 1.f / sum);
+        }
     }
 
     for (int c0 = 0; c0 < p.D; c0 += LPP * VEC) {
@@ -64,24 +70,32 @@ __global__ __launch_bounds__(kBlock) void fwd_kernel(Params p) {
         for (int k0 = 0; k0 < K; k0 += KC) {
             const int kn = K - k0 < KC ? K - k0 : KC;
             wave_lds_sync();
-            for (int j = lane; j < PPW * kn; j += 64) {
-                const int jq = j / kn, jk = j - jq * kn;
-                SampleDesc sd;
-                if constexpr (FUSED) {
-                    const int q = t.q0 + jq, k = k0 + jk;
-                    if (q < p.Lq) {
-                        const float2 st = s_stat[wave][jq];
-                        const float z = p.logits[((size_t)(t.n * p.Lq + q) * p.M + t.m) * K + k];
-                        describe_at(p, s_lvl, t.n, t.m, k, fused_location(p, s_lvl, t.n, t.m, q, k),
-                                    expf(z - st.x) * st.y, true, sd);
-                    } else {
-                        describe_at(p, s_lvl, t.n, t.m, k, make_float2(-2.f, -2.f), 0.f, true, sd);
+            if constexpr (FUSED) {
+                // every lane runs every pass, so that the in-pass softmax can reduce over groups of
+                // K lanes: with kn == K dividing 64 they are whole queries (or wholly past the items)
+                for (int j0 = 0; j0 < PPW * kn; j0 += 64) {
+                    const int j = j0 + lane, jq = j / kn, k = k0 + (j - jq * kn), q = t.q0 + jq;
+                    const bool item = j < PPW * kn, live = item && q < p.Lq;
+                    const float z = live ? p.logits[((size_t)(t.n * p.Lq + q) * p.M + t.m) * K + k] : 0.f;
+                    float2 st = make_float2(0.f, 0.f);
+                    if (softmax_in_pass) st = group_softmax_stats(z, K);
+                    else if (item) st = s_stat[wave][jq];
+                    if (item) {
+                        SampleDesc sd;
+                        const float2 xy = live ? fused_location(p, s_lvl, t.n, t.m, q, k) : make_float2(-2.f, -2.f);
+                        describe_at(p, s_lvl, t.n, t.m, k, xy, live ? expf(z - st.x) * st.y : 0.f, true, sd);
+                        s_off[wave][j] = sd.off;
+                        s_w[wave][j] = sd.w;
                     }
-                } else {
-                    describe(p, s_lvl, t.n, t.m, t.q0 + jq, k0 + jk, true, sd);
                 }
-                s_off[wave][j] = sd.off;
-                s_w[wave][j] = sd.w;
+            } else {
+                for (int j = lane; j < PPW * kn; j += 64) {
+                    const int jq = j / kn, jk = j - jq * kn;
+                    SampleDesc sd;
+                    describe(p, s_lvl, t.n, t.m, t.q0 + jq, k0 + jk, true, sd);
+                    s_off[wave][j] = sd.off;
+                    s_w[wave][j] = sd.w;
+                }
             }
             wave_lds_sync();
             if (active) {
