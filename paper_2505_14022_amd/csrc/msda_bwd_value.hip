@@ -104,15 +104,15 @@ __device__ __forceinline__ int level_of_tile(const int* g, int L, int tin) {
 
 // ---------------------------------------------------------------- 1. count
 
-constexpr int kBinRounds = kCountQueries / 256;  // samples per thread in the count / scatter passes
+constexpr int kBinRounds = kCountQueries / kBinBlock;  // samples per thread in the count / scatter passes
 
 // DET: the workgroup's histogram row goes to chunk_hist (no atomics), for placement in sample order.
 template <bool DET>
-__global__ __launch_bounds__(256) void bin_count_kernel(Params p) {
+__global__ __launch_bounds__(kBinBlock) void bin_count_kernel(Params p) {
     extern __shared__ int hist[];  // bins of this slab
     __shared__ int s_geo[kGeo * kMaxLevels];
     const int bps = p.bins_per_slab;
-    for (int i = threadIdx.x; i < bps; i += 256) hist[i] = 0;
+    for (int i = threadIdx.x; i < bps; i += kBinBlock) hist[i] = 0;
     load_geo(p, s_geo);
     const int slab = blockIdx.x / p.chunks, chunk = blockIdx.x - slab * p.chunks;
     const int n = slab / p.M, m = slab - n * p.M;
@@ -121,12 +121,12 @@ __global__ __launch_bounds__(256) void bin_count_kernel(Params p) {
     const int nsamp = nq * p.K;
     const float2* loc = reinterpret_cast<const float2*>(p.loc);
     // all of a thread's locations are loaded before any is binned, so their loads are in flight
-    // together (nsamp <= kCountQueries = 256 * kBinRounds)
+    // together (nsamp <= kCountQueries = kBinBlock * kBinRounds)
     float2 xy[kBinRounds];
     int lvl[kBinRounds];
 #pragma unroll
     for (int r = 0; r < kBinRounds; ++r) {
-        const int j = threadIdx.x + 256 * r;
+        const int j = threadIdx.x + kBinBlock * r;
         xy[r] = make_float2(-2.f, -2.f);  // off the map
         lvl[r] = 0;
         if (j < nsamp) {
@@ -143,10 +143,10 @@ __global__ __launch_bounds__(256) void bin_count_kernel(Params p) {
     __syncthreads();
     if constexpr (DET) {
         int* row = p.chunk_hist + (size_t)blockIdx.x * bps;
-        for (int i = threadIdx.x; i < bps; i += 256) row[i] = hist[i];
+        for (int i = threadIdx.x; i < bps; i += kBinBlock) row[i] = hist[i];
     } else {
         int* counts = p.counts + (size_t)slab * bps;
-        for (int i = threadIdx.x; i < bps; i += 256) {
+        for (int i = threadIdx.x; i < bps; i += kBinBlock) {
             const int c = hist[i];
             if (c) atomicAdd(&counts[i], c);
         }
@@ -429,7 +429,7 @@ __device__ __forceinline__ void scatter_chunk(const Params& p, const int* s_geo,
     int lvl[kBinRounds];
 #pragma unroll
     for (int r = 0; r < kBinRounds; ++r) {
-        const int j = threadIdx.x + 256 * r;
+        const int j = threadIdx.x + kBinBlock * r;
         xy[r] = make_float2(-2.f, -2.f);  // off the map
         lvl[r] = 0;
         rec[r] = make_int4(0, 0, 0, 0);
@@ -463,7 +463,7 @@ __device__ __forceinline__ void scatter_chunk(const Params& p, const int* s_geo,
         uint64_t peers[kBinRounds];
 #pragma unroll
         for (int r = 0; r < kBinRounds; ++r) peers[r] = peers_of(bins[r] < 0 ? 0 : bins[r], bits, __ballot(bins[r] >= 0));
-        for (int w = 0; w < kBlock / 64; ++w) {
+        for (int w = 0; w < kBinBlock / 64; ++w) {
             __syncthreads();
             if (wave == w) {
 #pragma unroll
@@ -483,11 +483,11 @@ __device__ __forceinline__ void scatter_chunk(const Params& p, const int* s_geo,
         __syncthreads();
         const int* base = p.chunk_hist + (size_t)blockIdx.x * bps;
         const int* off = p.offsets + (size_t)slab * bps;
-        for (int i = threadIdx.x; i < bps; i += 256) hist[i] = off[i] + base[i];
+        for (int i = threadIdx.x; i < bps; i += kBinBlock) hist[i] = off[i] + base[i];
     } else {
         __syncthreads();
         int* cursor = p.cursor + (size_t)slab * bps;
-        for (int i = threadIdx.x; i < bps; i += 256) {
+        for (int i = threadIdx.x; i < bps; i += kBinBlock) {
             const int c = hist[i];
             if (c) hist[i] = atomicAdd(&cursor[i], c);
         }
@@ -504,15 +504,16 @@ __device__ __forceinline__ void scatter_chunk(const Params& p, const int* s_geo,
 
 // Workgroups past n_slabs * chunks only prepare work items (below).
 template <bool DET>
-__global__ __launch_bounds__(256) void bin_scatter_kernel(Params p) {
+__global__ __launch_bounds__(kBinBlock) void bin_scatter_kernel(Params p) {
     extern __shared__ int hist[];  // bins of this slab
     __shared__ int s_geo[kGeo * kMaxLevels];
     const int bps = p.bins_per_slab;
-    for (int i = threadIdx.x; i < bps; i += 256) hist[i] = 0;
+    for (int i = threadIdx.x; i < bps; i += kBinBlock) hist[i] = 0;
     load_geo(p, s_geo);
     if (blockIdx.x < p.n_slabs * p.chunks) scatter_chunk<DET>(p, s_geo, hist, bps);
     // descriptors of the fold's work items (and zeroed rows of split tiles), a few tiles per wave
-    for (int t = blockIdx.x * 4 + (threadIdx.x >> 6); t < p.n_tiles; t += gridDim.x * 4)
+    constexpr int kPrepWaves = kBinBlock / 64;
+    for (int t = blockIdx.x * kPrepWaves + (threadIdx.x >> 6); t < p.n_tiles; t += gridDim.x * kPrepWaves)
         prep_tile(p, s_geo, t, threadIdx.x & 63);
 }
 
@@ -1471,12 +1472,12 @@ hipError_t launch_backward_value_binned(const Params& p0, msda_dtype_t dtype, hi
     const bool det = p.deterministic != 0;
     if (det && p.D % 4 != 0) return hipErrorNotSupported;
     if (det) {
-        hipLaunchKernelGGL(bin_count_kernel<true>, dim3(bin_blocks), dim3(256), hist_lds, stream, p);
+        hipLaunchKernelGGL(bin_count_kernel<true>, dim3(bin_blocks), dim3(kBinBlock), hist_lds, stream, p);
         if ((e = hipGetLastError()) != hipSuccess) return e;
         const int64_t cols = (int64_t)p.n_slabs * p.bins_per_slab;
         hipLaunchKernelGGL(chunk_scan_kernel, dim3((unsigned)((cols + 255) / 256)), dim3(256), 0, stream, p);
     } else {
-        hipLaunchKernelGGL(bin_count_kernel<false>, dim3(bin_blocks), dim3(256), hist_lds, stream, p);
+        hipLaunchKernelGGL(bin_count_kernel<false>, dim3(bin_blocks), dim3(kBinBlock), hist_lds, stream, p);
     }
     if ((e = hipGetLastError()) != hipSuccess) return e;
     hipLaunchKernelGGL(scan_reduce_kernel, dim3(p.scan_blocks), dim3(256), 0, stream, p);
@@ -1484,10 +1485,10 @@ hipError_t launch_backward_value_binned(const Params& p0, msda_dtype_t dtype, hi
     hipLaunchKernelGGL(scan_apply_kernel, dim3(p.scan_blocks), dim3(256), 0, stream, p);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     // the scatter's workgroups also prepare the work items, at least one wave per four tiles
-    const int prep_blocks = (p.n_tiles + 15) / 16;
+    const int prep_blocks = (p.n_tiles + 4 * (kBinBlock / 64) - 1) / (4 * (kBinBlock / 64));
     const dim3 scatter_grid(bin_blocks > prep_blocks ? bin_blocks : prep_blocks);
-    if (det) hipLaunchKernelGGL(bin_scatter_kernel<true>, scatter_grid, dim3(256), hist_lds, stream, p);
-    else hipLaunchKernelGGL(bin_scatter_kernel<false>, scatter_grid, dim3(256), hist_lds, stream, p);
+    if (det) hipLaunchKernelGGL(bin_scatter_kernel<true>, scatter_grid, dim3(kBinBlock), hist_lds, stream, p);
+    else hipLaunchKernelGGL(bin_scatter_kernel<false>, scatter_grid, dim3(kBinBlock), hist_lds, stream, p);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     if (p.D % 4 == 0) {
         const int grid = queue_grid(stream);  // the waves take work items from the queue

@@ -37,7 +37,10 @@ constexpr int kHistMax = 15872;      // bins of one (n, m) slab counted in LDS (
 constexpr int kTileFloats = 3200;    // LDS floats of one tile accumulator with its margin (12.5 KB per wave)
 constexpr int kBinnedMaxD = 355;     // channels per head handled by the binned path (1x1 tiles)
 constexpr int kChunkRecords = 512;   // records folded by one accumulate work item
-constexpr int kCountQueries = 4096;  // samples per workgroup in the counting / scatter passes
+// Threads per workgroup of the counting / scatter passes (512 or 1024, with four times the samples
+// per workgroup and so fewer bin atomics, made the backward 3-14 % slower), and their samples.
+constexpr int kBinBlock = 256;
+constexpr int kCountQueries = 16 * kBinBlock;
 constexpr int kScanTiles = 256;      // tiles per workgroup in the scan passes (one per thread)
 constexpr int kAtomicMaxSamples = 16384;  // problems this small take the atomic grad_value path
 // Bytes of the static device scratch of msda_backward_noalloc (per GPU, held until the process ends).
