@@ -42,6 +42,8 @@ VARIANTS = {
                     "pixels (variant: slab ranges on every shape)", ["detr_encoder", "bev_tsa_f16", "swin5_f16"]),
     "query_eighths": ("MSDA_ABLATE_QUERY_EIGHTHS", "slab ranges per XCD where the queries are fewer than half the value "
                       "pixels (variant: query eighths on every shape)", ["bev_sca", "detr_decoder"]),
+    "no_ksplit": ("MSDA_ABLATE_NO_KSPLIT", "small backward grids split each query chunk's samples over up to 8 "
+                  "workgroups (variant: one workgroup per query chunk)", ["detr_decoder"]),
     "vec1": ("MSDA_ABLATE_VEC1", "16-byte row pieces per lane (8 lanes x float4 per 128-byte row at D = 32)",
              ["detr_encoder"]),
     "no_dpp": ("MSDA_ABLATE_NO_DPP", "DPP lane permutations in the channel reductions (transposed corner sums)",

@@ -339,7 +339,11 @@ hipError_t launch_backward_grads(const Params& p0, msda_dtype_t dtype, bool atom
     // every output of a sample depends on that sample alone, so small grids may split a query's
     // samples over several workgroups; the fused chain rule needs all of them in one wave
     Params p = p0;
+#ifndef MSDA_ABLATE_NO_KSPLIT
     p.k_split_max = p.prologue_grads ? 1 : kMaxKSplit;
+#else
+    p.k_split_max = 1;
+#endif
     if (atomic_grad_value)
         return dtype == MSDA_F16 ? launch_typed<BwdAtomicK, _Float16>(p, stream)
                                  : launch_typed<BwdAtomicK, float>(p, stream);

@@ -14,6 +14,7 @@
 //                               (slab ranges on every shape)
 //   MSDA_ABLATE_SLAB_RANGES     slab ranges per XCD on every shape (no query eighths)
 //   MSDA_ABLATE_QUERY_EIGHTHS   query eighths per XCD on every shape
+//   MSDA_ABLATE_NO_KSPLIT       small backward grids keep each query chunk's samples in one workgroup
 //   MSDA_ABLATE_VEC1            one channel per lane (D lanes per query) instead of 16-byte pieces
 //   MSDA_ABLATE_NO_DPP          lane-group sums and maxima by ds_bpermute shuffles instead of DPP
 //   MSDA_ABLATE_PLAIN_STORES    outputs written with ordinary stores instead of nontemporal ones
