@@ -276,8 +276,9 @@ msda_status_t msda_backward_fused(const void* value, const int64_t* spatial_shap
                                   int64_t N, int64_t S, int64_t M, int64_t D, int64_t Lq, int64_t L,
                                   int64_t P, int dtype, void* stream);
 
-/* Static name of a status code ("MSDA_SUCCESS", ...). */
-const char* msda_status_string(msda_status_t status);
+/* Static name of a status code ("MSDA_SUCCESS", ...); any int is accepted, and a value that is no
+ * msda_status_t gives "MSDA_UNKNOWN_STATUS". */
+const char* msda_status_string(int status);
 
 /* Description of the last failed check or launch on the calling thread ("" if none). */
 const char* msda_last_error(void);

@@ -592,7 +592,7 @@ msda_status_t msda_backward_fused(const void* value, const int64_t* spatial_shap
                          binned ? ws + staging : nullptr, N, S, M, D, Lq, L, P, dtype, (hipStream_t)stream);
 }
 
-const char* msda_status_string(msda_status_t status) {
+const char* msda_status_string(int status) {
     switch (status) {
         case MSDA_SUCCESS: return "MSDA_SUCCESS";
         case MSDA_ERROR_INVALID_VALUE: return "MSDA_ERROR_INVALID_VALUE";
