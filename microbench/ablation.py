@@ -104,6 +104,7 @@ def step(cmd, env, log, limit):
 
 
 def run(out, variants):
+    out = os.path.abspath(out)  # the profiler runs from /tmp: relative output paths would land there
     os.makedirs(out, exist_ok=True)
     bench = [sys.executable, os.path.join(ROOT, "bench.py"), "--no-cpu-baseline", "--no-secondary"]
     for v in ["base"] + variants:
