@@ -40,6 +40,9 @@ VARIANTS = {
                      "chunk consecutive)", ["detr_encoder", "bev_tsa_f16"]),
     "slab_ranges": ("MSDA_ABLATE_SLAB_RANGES", "query eighths per XCD where the queries are at least half the value "
                     "pixels (variant: slab ranges on every shape)", ["detr_encoder", "bev_tsa_f16", "swin5_f16"]),
+    "index_eighths": ("MSDA_ABLATE_INDEX_EIGHTHS", "where there are as many queries as value pixels, the query eighths "
+                      "per XCD are bands of rows of every level (variant: eighths of the query index)",
+                      ["detr_encoder", "swin5_f16"]),
     "query_eighths": ("MSDA_ABLATE_QUERY_EIGHTHS", "slab ranges per XCD where the queries are fewer than half the value "
                       "pixels (variant: query eighths on every shape)", ["bev_sca", "detr_decoder"]),
     "no_ksplit": ("MSDA_ABLATE_NO_KSPLIT", "small backward grids split each query chunk's samples over up to 8 "

@@ -14,6 +14,8 @@
 //                               (slab ranges on every shape)
 //   MSDA_ABLATE_SLAB_RANGES     slab ranges per XCD on every shape (no query eighths)
 //   MSDA_ABLATE_QUERY_EIGHTHS   query eighths per XCD on every shape
+//   MSDA_ABLATE_INDEX_EIGHTHS   query eighths by query index also where there are as many queries as
+//                               value pixels (no bands of rows)
 //   MSDA_ABLATE_NO_KSPLIT       small backward grids keep each query chunk's samples in one workgroup
 //   MSDA_ABLATE_VEC1            one channel per lane (D lanes per query) instead of 16-byte pieces
 //   MSDA_ABLATE_NO_DPP          lane-group sums and maxima by ds_bpermute shuffles instead of DPP
@@ -70,6 +72,11 @@ struct Params {
     int k_split;           // bwd_kernel: a query chunk's samples are split over k_split work items
     int k_split_max;       // set by the launcher: the largest k_split it accepts (0 or 1: none)
     int xcd_split;         // forward / bwd_kernel work arrangement (tile_of): 1 query eighths, 0 slab ranges
+    int xcd_bands;         // with xcd_split: the eighths are bands of rows: XCD x takes the query chunks
+                           // whose first query lies in the x-th eighth of the rows of its level
+    int band_cap;          // with xcd_bands: work slots per slab and XCD
+    int band_count[8];     // with xcd_bands: query chunks of one slab that XCD x takes
+    int band_c[kMaxLevels][9];  // with xcd_bands: XCD x's chunks of level l are [band_c[l][x], band_c[l][x+1])
     int num_blocks;        // n_batch * M * chunks (the launch grid may be larger: see tile_of)
     int H[kMaxLevels], W[kMaxLevels], start[kMaxLevels];
     int stage_level;       // forward, MSDA_ABLATE_LDS_STAGE only: level staged in LDS (-1: none)

@@ -10,7 +10,8 @@ code launches it and as each lane forms its addresses:
   * the workgroup -> (batch, head, query chunk) arrangement over the eight XCDs: query eighths
     (XCD x takes the x-th eighth of every slab's query chunks) when there are at least half as many
     queries as value pixels, else slab ranges (XCD x takes a contiguous eighth of the slab-major
-    work items);
+    work items); with as many queries as value pixels the eighths are bands of rows (XCD x takes
+    the chunks whose first query lies in the x-th eighth of the rows of its level);
   * the sample split of small grids: a query chunk's K samples divided over up to 8 consecutive
     work items (at least 4 samples each, at most 4096 waves in all);
   * the per-sample description: fp32 image coordinates, the open range test, floor, the int32
@@ -91,13 +92,35 @@ class Launch:
     grid: int
     split: bool
     k_split: int
+    bands: bool = False
+    band_c: tuple = ()      # band_c[l][x]: first chunk of level l in band x (x = 0..8)
+    band_count: tuple = ()  # chunks of one slab in band x
+    band_cap: int = 0
 
 
 class AddressError(AssertionError):
     pass
 
 
-def launches(N, S, M, D, Lq, L, P, es):
+def band_table(shapes, qpb):
+    """Chunk ranges of the bands of rows: row h of level l is in band floor(8 (h + 1/2) / H_l), and a
+    query chunk goes with the band of its first query (query q is pixel q in level-major order)."""
+    first_chunk = lambda q: (q + qpb - 1) // qpb
+    start, bc = 0, []
+    for H, W in shapes:
+        row = []
+        for x in range(8):
+            r0 = max(0, -(-(x * H - 4) // 8))  # first row with 8 h + 4 >= x H
+            row.append(first_chunk(start + r0 * W))
+        start += H * W
+        row.append(first_chunk(start))
+        bc.append(tuple(row))
+    count = tuple(sum(r[x + 1] - r[x] for r in bc) for x in range(8))
+    return tuple(bc), count, max(count)
+
+
+def launches(N, S, M, D, Lq, L, P, es, shapes=None):
+    """The launches of the backward kernel; `shapes` ((H, W) per level) is needed where Lq == S."""
     nb = batch_per_launch(S, M, D, Lq, L, P)
     vec = pick_vec(D, es)
     lpp = pick_lpp(D, vec)
@@ -118,7 +141,15 @@ def launches(N, S, M, D, Lq, L, P, es):
         split_grid = 8 * cnt * M * ((chunks + 7) // 8)
         split = 2 * Lq >= S and split_grid <= MAX_INDEX
         grid = split_grid if split else (num_blocks + 7) // 8 * 8
-        out.append(Launch(n0, cnt, vec, lpp, ppw, waves, qpb, chunks, num_blocks, grid, split, ks))
+        ln = Launch(n0, cnt, vec, lpp, ppw, waves, qpb, chunks, num_blocks, grid, split, ks)
+        if split and ks == 1 and Lq == S:
+            if shapes is None:
+                raise ValueError("the band arrangement needs the level shapes")
+            bc, count, cap = band_table(shapes, qpb)
+            band_grid = 8 * cnt * M * cap
+            if band_grid <= MAX_INDEX:
+                ln.bands, ln.band_c, ln.band_count, ln.band_cap, ln.grid = True, bc, count, cap, band_grid
+        out.append(ln)
     return out
 
 
@@ -135,7 +166,19 @@ def wave_queries(ln: Launch, M: int):
     chunk / k_split, sample part chunk % k_split."""
     b = np.arange(ln.grid, dtype=np.int64)
     x, i = b & 7, b >> 3
-    if ln.split:
+    if ln.bands:
+        slab, k = i // ln.band_cap, i % ln.band_cap
+        keep = (slab < ln.cnt * M) & (k < np.asarray(ln.band_count)[x])
+        slab, k, xs = slab[keep], k[keep], x[keep]
+        chunk = np.full(slab.shape, -1, dtype=np.int64)
+        for l, row in enumerate(ln.band_c):
+            row = np.asarray(row)
+            c0, n = row[xs], row[xs + 1] - row[xs]
+            take = (chunk < 0) & (k < n)
+            chunk[take] = (c0 + k)[take]
+            k = np.where(chunk < 0, k - n, k)
+        _check(chunk >= 0, "band slot past its chunks")
+    elif ln.split:
         per = (ln.chunks + 7) // 8
         slab = i // per
         chunk = ((x * ln.chunks) >> 3) + i % per
@@ -224,7 +267,7 @@ def model_atomic_backward(value, shapes, starts, loc, attn, grad_out, plant_col_
     g = np.asarray(grad_out, dtype=np.float64).reshape(N * Lq * M, D)
     stats = {"launches": 0, "sample_slots": 0, "tail_slots": 0, "corner_atomics_landed": 0,
              "corner_atomics_dropped": 0}
-    lns = launches(N, S, M, D, Lq, L, P, es)
+    lns = launches(N, S, M, D, Lq, L, P, es, shapes=list(zip(H, W)))
     for ln in lns:
         stats["launches"] += 1
         loads, atom = lane_channel_maps(D, ln.vec, ln.lpp)

@@ -28,6 +28,13 @@ SMALL = [
     (2, 3, 33, ((10, 10), (5, 5)), 3, 77, "f32"),
 ]
 
+# as many queries as value pixels: the band arrangement (when the grid is large enough not to
+# split samples)
+BANDS = [
+    (2, 4, 32, ((20, 30), (10, 15), (5, 8)), 4, 20 * 30 + 10 * 15 + 5 * 8, "f32"),
+    (1, 8, 32, ((33, 17), (9, 9)), 2, 33 * 17 + 81, "f16"),
+]
+
 
 def _compare(inp):
     gv, stats = model_atomic_backward(inp.value, inp.shapes, inp.starts, inp.loc, inp.attn, inp.grad_out)
@@ -40,7 +47,7 @@ def _compare(inp):
     return stats
 
 
-@pytest.mark.parametrize("case", SMALL, ids=lambda c: f"N{c[0]}M{c[1]}D{c[2]}L{len(c[3])}P{c[4]}Lq{c[5]}{c[6]}")
+@pytest.mark.parametrize("case", SMALL + BANDS, ids=lambda c: f"N{c[0]}M{c[1]}D{c[2]}L{len(c[3])}P{c[4]}Lq{c[5]}{c[6]}")
 def test_small_cases(case):
     N, M, D, shapes, P, Lq, dt = case
     _compare(workloads.random_case(N, M, D, shapes, P, Lq, dt, seed=1000 + D + Lq))
@@ -75,19 +82,37 @@ def test_model_catches_a_planted_offset_error(step):
                               plant_col_step=step)
 
 
-def test_both_xcd_arrangements_are_modelled():
-    # query eighths where queries are at least half the value pixels, slab ranges elsewhere; the
-    # cases above exercise both
+def _arrangements(N, M, D, shapes, P, Lq, dt):
     from kernel_model import launches
 
-    def split(N, M, D, shapes, P, Lq, dt):
-        S = sum(h * w for h, w in shapes)
-        return {ln.split for ln in launches(N, S, M, D, Lq, len(shapes), P, 2 if dt == "f16" else 4)}
+    S = sum(h * w for h, w in shapes)
+    lns = launches(N, S, M, D, Lq, len(shapes), P, 2 if dt == "f16" else 4, shapes=shapes)
+    return {"bands" if ln.bands else "eighths" if ln.split else "slabs" for ln in lns}
 
-    assert {True, False} <= set().union(*(split(*c) for c in SMALL))
+
+def test_every_xcd_arrangement_is_modelled():
+    # bands of rows where there are as many queries as value pixels, query eighths where there are
+    # at least half as many, slab ranges elsewhere; the cases above exercise all three
+    assert {"bands", "eighths", "slabs"} <= set().union(*(_arrangements(*c) for c in SMALL + BANDS))
     enc, dec = workloads.BY_NAME["detr_encoder"], workloads.BY_NAME["detr_decoder"]
-    assert split(enc.N, enc.M, enc.D, enc.shapes, enc.P, enc.Lq, enc.dtype) == {True}
-    assert split(dec.N, dec.M, dec.D, dec.shapes, dec.P, dec.Lq, dec.dtype) == {False}
+    assert _arrangements(enc.N, enc.M, enc.D, enc.shapes, enc.P, enc.Lq, enc.dtype) == {"bands"}
+    assert _arrangements(dec.N, dec.M, dec.D, dec.shapes, dec.P, dec.Lq, dec.dtype) == {"slabs"}
+
+
+def test_band_table_partitions_the_chunks():
+    # every query chunk of a level-major pixel order lands in exactly one (level, band) range, and the
+    # bands of a level are contiguous and ordered
+    from kernel_model import band_table
+
+    rng = np.random.default_rng(3)
+    for _ in range(200):
+        shapes = [tuple(int(v) for v in rng.integers(1, 70, size=2)) for _ in range(int(rng.integers(1, 6)))]
+        qpb = int(rng.choice([1, 2, 8, 16, 32, 64, 256]))
+        S = sum(h * w for h, w in shapes)
+        bc, count, cap = band_table(shapes, qpb)
+        chunks = [c for row in bc for x in range(8) for c in range(row[x], row[x + 1])]
+        assert sorted(chunks) == list(range((S + qpb - 1) // qpb))
+        assert sum(count) == len(chunks) and cap == max(count)
 
 
 def test_small_grids_split_samples():
@@ -95,5 +120,5 @@ def test_small_grids_split_samples():
     # the encoder's grid is large enough as it is
     from kernel_model import launches
     dec, enc = workloads.BY_NAME["detr_decoder"], workloads.BY_NAME["detr_encoder"]
-    assert {ln.k_split for ln in launches(dec.N, dec.S, dec.M, dec.D, dec.Lq, dec.L, dec.P, 4)} == {4}
-    assert {ln.k_split for ln in launches(enc.N, enc.S, enc.M, enc.D, enc.Lq, enc.L, enc.P, 4)} == {1}
+    assert {ln.k_split for ln in launches(dec.N, dec.S, dec.M, dec.D, dec.Lq, dec.L, dec.P, 4, dec.shapes)} == {4}
+    assert {ln.k_split for ln in launches(enc.N, enc.S, enc.M, enc.D, enc.Lq, enc.L, enc.P, 4, enc.shapes)} == {1}
