@@ -160,9 +160,10 @@ def _check(cond, msg):
 
 def wave_queries(ln: Launch, M: int):
     """(n, m, q, part) of every query slot of every wave of the launch, in the kernel's mapping:
-    with x = b % 8 and i = b / 8, workgroup b runs chunk x*chunks/8 + i % per of slab i / per
-    (query eighths, per = ceil(chunks / 8)) or work item w = x * (G / 8) + i in slab-major order
-    (slab ranges). Every (slab, chunk) must be run exactly once; a work item is query chunk
+    with x = b % 8 and i = b / 8, workgroup b runs the (i % cap)-th chunk of band x of slab i / cap
+    (bands of rows: the chunks of band x, level after level), chunk x*chunks/8 + i % per of slab
+    i / per (query eighths, per = ceil(chunks / 8)) or work item w = x * (G / 8) + i in slab-major
+    order (slab ranges). Every (slab, chunk) must be run exactly once; a work item is query chunk
     chunk / k_split, sample part chunk % k_split."""
     b = np.arange(ln.grid, dtype=np.int64)
     x, i = b & 7, b >> 3
