@@ -51,6 +51,28 @@ def test_small_parity(case, path):
     check_parity(inp, workspace="owner" if path == "owner" else None)
 
 
+# As many queries as value pixels, each query at its own pixel (encoder self-attention): the forward
+# and backward kernels deal the query chunks to the XCDs in bands of rows of every level. Row counts
+# that do not divide by 8 leave bands of different sizes (workgroups past the end of a band exit);
+# the grids are large enough that the backward does not split samples (which would use eighths of
+# the query index instead).
+BANDS = [
+    ("detr_encoder", 2, ((40, 60), (20, 30), (10, 15), (5, 8))),
+    ("swin5_f16", 2, ((66, 80), (33, 40), (17, 20), (9, 10), (5, 5))),
+    ("bev_tsa_f16", 8, ((45, 37),)),
+]
+
+
+@pytest.mark.parametrize("path", ["owner", "atomic"])
+@pytest.mark.parametrize("case", BANDS, ids=lambda c: f"{c[0]}_N{c[1]}_S{sum(h * w for h, w in c[2])}")
+def test_band_arrangement(case, path):
+    base, N, shapes = case
+    S = sum(h * w for h, w in shapes)
+    w = workloads.scaled(workloads.BY_NAME[base], N=N, Lq=S, shapes=shapes, name=f"{base}_bands_N{N}_S{S}")
+    say(f"bands of rows: {w.name} ({path} grad_value)")
+    check_parity(workloads.generate(w), workspace="owner" if path == "owner" else None)
+
+
 @pytest.mark.parametrize("seed", range(3))
 def test_dense_coarse_levels_split_tiles(seed):
     # many queries on small maps: tiles see more samples than one work item folds, so tiles are
