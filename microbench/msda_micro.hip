@@ -1,9 +1,11 @@
 // Microbenchmarks behind the kernel design (gfx950, one GPU), in the manner of the paper's
 // Sec. 3 measurements of gather and scatter rates (Fig. 4-5), for this chip:
 //   1. gather ceiling: the forward's access pattern alone at the DETR-encoder shape (four 128-byte
-//      corner rows per sample, 8 lanes x 16 bytes per row, 8 queries per wave, one (batch, head)
-//      slab per XCD), with the per-sample descriptions read from memory instead of computed;
-//      variants: two corners only, the [N, M, S, D] layout, L1-bypassing loads;
+//      corner rows per sample, 8 lanes x 16 bytes per row, 8 queries per wave), with the per-sample
+//      descriptions read from memory instead of computed; work dealt to the XCDs as the forward
+//      deals it (bands of rows, two samples in flight per lane) or in slab ranges (one (batch, head)
+//      slab per XCD, four samples in flight); variants: two corners only, the [N, M, S, D] layout,
+//      L1-bypassing loads;
 //   2. fp32 device atomics: rows covered by whole instructions (32 lanes per 128-byte row), eight
 //      32-byte row pieces per instruction, 64 scattered dwords; u32 for comparison;
 //   3. LDS accumulation: ds_add_f32, a compare-and-swap loop, ds_add_f64, a plain
@@ -43,13 +45,59 @@ constexpr int kLq = kS;
 constexpr uint32_t kOOB = 0x7fffffffu;  // byte offset past every buffer: the load returns zero
 
 // ------------------------------------------------------------------------- 1. gather ceiling
+// Bands of rows: XCD x takes the 32-query chunks whose first query lies in the x-th eighth of the rows
+// of its level; XCD x's chunks of level l are [c[l][x], c[l][x + 1]).
+struct Bands {
+    int c[kL][9];
+    int count[8];
+    int cap;
+};
+
+Bands make_bands() {
+    Bands bd = {};
+    int s = 0;
+    for (int l = 0; l < kL; ++l) {
+        for (int x = 0; x < 8; ++x) {
+            const int a = x * kH[l] - 4;  // first row h with 8 h + 4 >= x H
+            const int r0 = a > 0 ? (a + 7) / 8 : 0;
+            bd.c[l][x] = (s + r0 * kW[l] + 31) / 32;
+        }
+        s += kH[l] * kW[l];
+        bd.c[l][8] = (s + 31) / 32;
+    }
+    for (int x = 0; x < 8; ++x) {
+        for (int l = 0; l < kL; ++l) bd.count[x] += bd.c[l][x + 1] - bd.c[l][x];
+        if (bd.count[x] > bd.cap) bd.cap = bd.count[x];
+    }
+    return bd;
+}
+
 // desc[slab][q][k]: the four corner pixels of sample k of query q (-1: off the map)
-template <int LAYOUT, int CORNERS, int AUX>
-__global__ __launch_bounds__(256) void gather(const float* value, const int4* desc, float* out, int chunks) {
+template <int LAYOUT, int CORNERS, int AUX, int MAP, int U>
+__global__ __launch_bounds__(256) void gather(const float* value, const int4* desc, float* out, int chunks, Bands bd) {
     const uint32_t G = gridDim.x, b = blockIdx.x;
-    const uint32_t w = (b & 7u) * (G >> 3) + (b >> 3);  // slab-major work, dealt to XCDs in turn
-    if (w >= (uint32_t)(kN * kM * chunks)) return;
-    const int slab = (int)w / chunks, chunk = (int)w - slab * chunks;
+    int slab, chunk;
+    if (MAP == 1) {
+        const int x = (int)(b & 7u), i = (int)(b >> 3);
+        slab = i / bd.cap;
+        int k = i - slab * bd.cap;
+        if (slab >= kN * kM || k >= bd.count[x]) return;
+        chunk = -1;
+        for (int l = 0; l < kL; ++l) {
+            const int n = bd.c[l][x + 1] - bd.c[l][x];
+            if (k < n) {
+                chunk = bd.c[l][x] + k;
+                break;
+            }
+            k -= n;
+        }
+        if (chunk < 0) return;
+    } else {
+        const uint32_t w = (b & 7u) * (G >> 3) + (b >> 3);  // slab-major work, dealt to XCDs in turn
+        if (w >= (uint32_t)(kN * kM * chunks)) return;
+        slab = (int)w / chunks;
+        chunk = (int)w - slab * chunks;
+    }
     const int n = slab / kM, m = slab - n * kM;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int q = chunk * 32 + wave * 8 + lane / 8, sub = lane & 7;
@@ -69,7 +117,7 @@ __global__ __launch_bounds__(256) void gather(const float* value, const int4* de
         acc.z += __builtin_bit_cast(float, u2);
         acc.w += __builtin_bit_cast(float, u3);
     };
-#pragma unroll 4
+#pragma unroll U
     for (int k = 0; k < kK; ++k) {
         const int4 c = d[k];
         add(__builtin_amdgcn_raw_buffer_load_b128(vr, addr(c.x), 0, AUX));
@@ -82,19 +130,20 @@ __global__ __launch_bounds__(256) void gather(const float* value, const int4* de
     reinterpret_cast<float4*>(out)[((size_t)(n * kLq + q) * kM + m) * 8 + sub] = acc;
 }
 
-template <int LAYOUT, int CORNERS, int AUX>
+template <int LAYOUT, int CORNERS, int AUX, int MAP, int U>
 void run_gather(const char* name, const float* value, const int4* desc, float* out, double valid_frac) {
     const int chunks = (kLq + 31) / 32;
-    const int blocks = (kN * kM * chunks + 7) / 8 * 8;
+    const Bands bd = make_bands();
+    const int blocks = MAP == 1 ? 8 * kN * kM * bd.cap : (kN * kM * chunks + 7) / 8 * 8;
     hipEvent_t a, b;
     CK(hipEventCreate(&a));
     CK(hipEventCreate(&b));
-    for (int i = 0; i < 5; ++i) hipLaunchKernelGGL((gather<LAYOUT, CORNERS, AUX>), dim3(blocks), dim3(256), 0, 0, value, desc, out, chunks);
+    for (int i = 0; i < 5; ++i) hipLaunchKernelGGL((gather<LAYOUT, CORNERS, AUX, MAP, U>), dim3(blocks), dim3(256), 0, 0, value, desc, out, chunks, bd);
     CK(hipGetLastError());
     CK(hipDeviceSynchronize());
     constexpr int R = 30;
     CK(hipEventRecord(a));
-    for (int i = 0; i < R; ++i) hipLaunchKernelGGL((gather<LAYOUT, CORNERS, AUX>), dim3(blocks), dim3(256), 0, 0, value, desc, out, chunks);
+    for (int i = 0; i < R; ++i) hipLaunchKernelGGL((gather<LAYOUT, CORNERS, AUX, MAP, U>), dim3(blocks), dim3(256), 0, 0, value, desc, out, chunks, bd);
     CK(hipEventRecord(b));
     CK(hipEventSynchronize(b));
     float ms = 0.f;
@@ -276,11 +325,13 @@ int main() {
     CK(hipMalloc(&ddesc, desc.size() * sizeof(int4)));
     CK(hipMemcpy(ddesc, desc.data(), desc.size() * sizeof(int4), hipMemcpyHostToDevice));
     CK(hipMemset(value, 0, vbytes));
-    run_gather<0, 4, 0>("4 corners, [N,S,M,D] (the forward's)", value, ddesc, out, vf);
-    run_gather<0, 2, 0>("2 corners, [N,S,M,D]", value, ddesc, out, vf);
-    run_gather<1, 4, 0>("4 corners, [N,M,S,D]", value, ddesc, out, vf);
-    run_gather<0, 4, 1>("4 corners, [N,S,M,D], sc0 loads", value, ddesc, out, vf);
-    run_gather<0, 4, 0>("4 corners, [N,S,M,D] (repeat)", value, ddesc, out, vf);
+    run_gather<0, 4, 0, 1, 2>("4 corners, bands, 2 in flight (forward's)", value, ddesc, out, vf);
+    run_gather<0, 4, 0, 0, 2>("4 corners, slab ranges, 2 in flight", value, ddesc, out, vf);
+    run_gather<0, 4, 0, 0, 4>("4 corners, [N,S,M,D], slab ranges", value, ddesc, out, vf);
+    run_gather<0, 2, 0, 0, 4>("2 corners, [N,S,M,D]", value, ddesc, out, vf);
+    run_gather<1, 4, 0, 0, 4>("4 corners, [N,M,S,D]", value, ddesc, out, vf);
+    run_gather<0, 4, 1, 0, 4>("4 corners, [N,S,M,D], sc0 loads", value, ddesc, out, vf);
+    run_gather<0, 4, 0, 1, 2>("4 corners, bands (repeat)", value, ddesc, out, vf);
     CK(hipFree(value));
     CK(hipFree(out));
     CK(hipFree(ddesc));
