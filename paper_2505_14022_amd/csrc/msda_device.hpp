@@ -359,32 +359,6 @@ inline bool xcd_bands(const Params& p) {
 #endif
 }
 
-// The chunk ranges of xcd_bands: row h of level l is in band floor(8 (h + 1/2) / H_l), and a query
-// chunk goes with the band of its first query.
-inline void set_bands(Params& p) {
-    const int64_t qpb = p.q_per_block;
-    auto first_chunk = [&](int64_t q) { return (int)((q + qpb - 1) / qpb); };
-    for (int l = 0; l < kMaxLevels; ++l)
-        for (int x = 0; x <= 8; ++x) p.band_c[l][x] = 0;
-    for (int l = 0; l < p.L; ++l) {
-        const int64_t H = p.H[l], W = p.W[l], s = p.start[l];
-        for (int x = 0; x < 8; ++x) {
-            // first row whose band is at least x: 8 h + 4 >= x H
-            int64_t r0 = (x * H - 4 + 7) / 8;
-            if (x * H - 4 <= 0) r0 = 0;
-            p.band_c[l][x] = first_chunk(s + r0 * W);
-        }
-        p.band_c[l][8] = first_chunk(s + H * W);
-    }
-    p.band_cap = 0;
-    for (int x = 0; x < 8; ++x) {
-        int n = 0;
-        for (int l = 0; l < p.L; ++l) n += p.band_c[l][x + 1] - p.band_c[l][x];
-        p.band_count[x] = n;
-        if (n > p.band_cap) p.band_cap = n;
-    }
-}
-
 // Per-sample description computed in phase 1.
 struct SampleDesc {
     int4 off;    // element offsets of the four corner rows (channel 0), or kOOBElem

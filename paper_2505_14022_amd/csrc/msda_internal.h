@@ -113,6 +113,10 @@ struct Params {
     float* partials;            // [max_items][64][D]  (deterministic) sums of the work items of split tiles
 };
 
+// The chunk ranges of the band arrangement (p.xcd_bands) for p.q_per_block queries per chunk: fills
+// p.band_c, p.band_count and p.band_cap from the level table (host code).
+void set_bands(Params& p);
+
 hipError_t launch_forward(const Params& p, msda_dtype_t dtype, hipStream_t stream);
 // The forward with locations and weights computed from ref / offsets / logits.
 hipError_t launch_forward_fused(const Params& p, msda_dtype_t dtype, hipStream_t stream);

@@ -3,7 +3,8 @@
 // Built by tests/test_host_sanitize.py with the sanitizers on the host code only. Everything called
 // here runs on the host and makes no GPU call: the argument checks, the workspace sizing (the
 // owner-computes plan: tile sizes, bins, work items and byte counts per level), the error paths of
-// every entry point that reject a call before anything is enqueued, and the status strings.
+// every entry point that reject a call before anything is enqueued, the chunk table of the band
+// arrangement of the forward and backward kernels, and the status strings.
 // Random problems come from a fixed-seed generator; the program prints one line per group of
 // checks and exits non-zero if a check fails (a sanitizer report aborts it).
 #include <cstdint>
@@ -11,6 +12,7 @@
 #include <vector>
 
 #include "msda.h"
+#include "msda_internal.h"
 
 namespace {
 
@@ -154,7 +156,47 @@ int main() {
                             nullptr) == MSDA_ERROR_INVALID_VALUE, "forward bad table", 0);
     }
 
-    // 4. status strings and the version
+    // 4. the band arrangement's chunk table: every query chunk of a level-major pixel order lies in exactly
+    //    one (level, band) range, the band of its first query's row floor(8 (h + 1/2) / H), counted in its
+    //    band; checked by brute force over random level tables and chunk sizes
+    int tables = 0;
+    for (int i = 0; i < kProblems; ++i) {
+        const Problem pr = random_problem();
+        msda::Params p = {};
+        p.L = (int)pr.L;
+        for (int64_t l = 0; l < pr.L; ++l) {
+            p.H[l] = (int)pr.shapes[2 * l];
+            p.W[l] = (int)pr.shapes[2 * l + 1];
+            p.start[l] = (int)pr.starts[l];
+        }
+        p.q_per_block = 1 << uniform(0, 8);
+        msda::set_bands(p);
+        const int64_t qpb = p.q_per_block, chunks = (pr.S + qpb - 1) / qpb;
+        std::vector<int> band(chunks, -1);
+        int counted[8] = {0}, cap = 0;
+        bool ok = true;
+        for (int l = 0; l < p.L && ok; ++l)
+            for (int x = 0; x < 8 && ok; ++x)
+                for (int c = p.band_c[l][x]; c < p.band_c[l][x + 1] && ok; ++c) {
+                    const int64_t q = c * qpb, rel = q - p.start[l];
+                    ok = c >= 0 && c < chunks && band[c] < 0 && rel >= 0 && rel < (int64_t)p.H[l] * p.W[l] &&
+                         (8 * (rel / p.W[l]) + 4) / p.H[l] == x;
+                    if (ok) {
+                        band[c] = x;
+                        ++counted[x];
+                    }
+                }
+        for (int64_t c = 0; c < chunks && ok; ++c) ok = band[c] >= 0;
+        for (int x = 0; x < 8 && ok; ++x) {
+            ok = counted[x] == p.band_count[x];
+            if (counted[x] > cap) cap = counted[x];
+        }
+        expect(ok && cap == p.band_cap, "band table partitions the query chunks", i);
+        tables += ok;
+    }
+    std::printf("band tables checked: %d of %d\n", tables, kProblems);
+
+    // 5. status strings and the version
     for (int s = -1; s <= 4; ++s) expect(msda_status_string(s) != nullptr, "status string", s);
     expect(msda_version() > 0, "version", 0);
 

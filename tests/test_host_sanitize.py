@@ -3,7 +3,8 @@
 tests/host_sanitize.cpp is linked with every library source, the sanitizers applied to the host
 code only (the device code is built as usual and never launched), and run: argument checks and
 workspace sizing over random valid and invalid problems, the host-side rejection of every entry
-point, and the status strings. No call reaches the GPU.
+point, the chunk table of the band arrangement against a brute-force assignment, and the status
+strings. No call reaches the GPU.
 """
 import os
 import shutil
@@ -37,3 +38,4 @@ def test_host_code_under_sanitizers(tmp_path):
     assert run.returncode == 0, out[-4000:]
     assert "runtime error" not in out and "AddressSanitizer" not in out, out[-4000:]
     assert "failures: 0" in run.stdout
+    assert "band tables checked: 400 of 400" in run.stdout, run.stdout[-2000:]
