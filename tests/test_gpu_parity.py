@@ -54,12 +54,14 @@ def test_small_parity(case, path):
 # As many queries as value pixels, each query at its own pixel (encoder self-attention): the forward
 # and backward kernels deal the query chunks to the XCDs in bands of rows of every level. Row counts
 # that do not divide by 8 leave bands of different sizes (workgroups past the end of a band exit);
-# the grids are large enough that the backward does not split samples (which would use eighths of
-# the query index instead).
+# the first three grids are large enough that the backward does not split samples (which would use
+# eighths of the query index instead); the last one is not.
 BANDS = [
     ("detr_encoder", 2, ((40, 60), (20, 30), (10, 15), (5, 8))),
     ("swin5_f16", 2, ((66, 80), (33, 40), (17, 20), (9, 10), (5, 5))),
     ("bev_tsa_f16", 8, ((45, 37),)),
+    # a small grid: the forward takes the bands, the backward splits samples and takes query eighths
+    ("detr_encoder", 1, ((12, 10), (6, 5))),
 ]
 
 
